@@ -1,0 +1,262 @@
+/*
+ * sllm.h — C ABI of the MI355X checkpoint loader.
+ *
+ * The library converts a tensor checkpoint into a loading-optimized format
+ * and streams it from pinned host DRAM into one preallocated HBM buffer
+ * (ServerlessLLM, Sec. 4, fast multi-tier checkpoint loading).
+ *
+ * Format (Sec. 4.1).  A checkpoint directory holds two files:
+ *   sllm.part0  the partition for one GPU: the tensors' bytes only, in the
+ *               caller's order, each at an offset aligned to A (a power of
+ *               two), zero padding between tensors, zero-filled up to
+ *               F = align_up(T, 4096) bytes, where T = sum align_up(s_i, A).
+ *   sllm.index  the tensor index: name -> (dtype, shape, partition, offset,
+ *               size), little-endian, closed by a CRC-32 (IEEE).  The exact
+ *               byte layout is in docs/FORMAT.md.
+ * A tensor's device address is base + offset (Sec. 4.1, direct tensor
+ * addressing).
+ *
+ * Loading (Sec. 4.2).  Chunk k of a partition is the byte range
+ * [kC, min(kC + C, T)).  Chunks move through a pool of fixed-size pinned host
+ * chunks (the DRAM tier, with allocate/evict calls under application control)
+ * and from there into device memory, either by the copy (SDMA) engines or by
+ * a gfx950 kernel that reads the mapped host chunks directly.
+ *
+ * Conventions.
+ *   - Every call returns an int32_t status: SLLM_OK (0) or a negative
+ *     SLLM_E_* code; sllm_last_error() then gives a message for this thread.
+ *   - No C++ exception crosses this interface.
+ *   - "Device pointer" means an address in the HIP device's memory (for
+ *     example a torch uint8 CUDA tensor's data_ptr()); "stream" is a
+ *     hipStream_t passed as void* (NULL = the null stream).
+ *   - The caller owns every buffer and stream it passes in.  The library
+ *     owns its handles and everything reachable from them until the matching
+ *     close/destroy call.
+ *   - A handle may be used by one thread at a time; different handles may
+ *     be used from different threads.
+ */
+#ifndef SLLM_H
+#define SLLM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes -------------------------------------------------------- */
+#define SLLM_OK          0
+#define SLLM_E_INVAL    -1  /* bad argument or option                           */
+#define SLLM_E_IO       -2  /* a file could not be opened, read or written      */
+#define SLLM_E_FORMAT   -3  /* index or partition damaged or inconsistent       */
+#define SLLM_E_NOMEM    -4  /* host or pool memory exhausted                    */
+#define SLLM_E_HIP      -5  /* a HIP runtime call failed                        */
+#define SLLM_E_RANGE    -6  /* destination buffer too small                     */
+#define SLLM_E_BUSY     -7  /* object in use (load in progress, cached, opened) */
+#define SLLM_E_NOTFOUND -8  /* no such tensor / checkpoint                      */
+
+/* ---- dtypes (stored bytes are never converted) ---------------------------- */
+#define SLLM_DTYPE_F32  0
+#define SLLM_DTYPE_F16  1
+#define SLLM_DTYPE_BF16 2
+#define SLLM_DTYPE_I8   3
+#define SLLM_MAX_NDIM   8
+
+/* =========================================================================
+ * Conversion (Sec. 4.1: checkpoints are converted once, loaded many times)
+ * ========================================================================= */
+
+/* One tensor of the source checkpoint.  `data` holds `nbytes` raw
+ * little-endian bytes, and nbytes must equal prod(shape) * itemsize(dtype)
+ * (a 0-d tensor has one element).  `name` is non-empty UTF-8 of at most
+ * 65535 bytes, unique within the checkpoint. */
+typedef struct sllm_src_tensor {
+    const char*    name;
+    uint32_t       dtype;   /* SLLM_DTYPE_* */
+    uint32_t       ndim;    /* 0 .. SLLM_MAX_NDIM */
+    const int64_t* shape;   /* ndim entries, each >= 0 (may be NULL if ndim == 0) */
+    const void*    data;    /* host memory; may be NULL if nbytes == 0 */
+    uint64_t       nbytes;
+} sllm_src_tensor;
+
+#define SLLM_CONVERT_FSYNC 1u   /* fsync both files before returning */
+
+typedef struct sllm_convert_opts {
+    uint64_t alignment;   /* A: power of two >= 1; 0 means 256            */
+    uint64_t chunk_size;  /* default load chunk size C >= 1; 0 means 16 MiB */
+    uint32_t flags;       /* SLLM_CONVERT_*                                */
+    uint32_t reserved;    /* must be 0                                     */
+} sllm_convert_opts;
+
+/* Write out_dir/sllm.part0 and out_dir/sllm.index for the n tensors, in the
+ * given order (out_dir must exist).  opts may be NULL (A = 256, C = 16 MiB).
+ * The caller's tensor memory is only read during the call.  Existing files
+ * are replaced; on error both files are removed.
+ * Errors: INVAL (bad tensor or option; duplicate or empty name), IO. */
+int32_t sllm_convert(const sllm_src_tensor* tensors, uint64_t n,
+                     const char* out_dir, const sllm_convert_opts* opts);
+
+/* Streaming form of sllm_convert for checkpoints that do not fit in host
+ * memory twice: tensors are added one at a time and written immediately.
+ * The files it produces are byte-identical to sllm_convert's.
+ * sllm_writer_close writes the index and frees the writer (even on error);
+ * sllm_writer_abort removes the partial files and frees the writer. */
+typedef struct sllm_writer sllm_writer;
+int32_t sllm_writer_open(const char* out_dir, const sllm_convert_opts* opts,
+                         sllm_writer** out);
+int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* tensor);
+int32_t sllm_writer_close(sllm_writer* w);
+void    sllm_writer_abort(sllm_writer* w);
+
+/* =========================================================================
+ * Pinned host chunk pool: the DRAM tier (Sec. 4.2, chunk-based data
+ * management: fixed-size chunks, allocation and eviction under the
+ * application's control)
+ * ========================================================================= */
+
+typedef struct sllm_pool sllm_pool;
+
+/* Allocate n_chunks pinned, device-mapped host chunks of chunk_size bytes
+ * (>= 1) for HIP device `device`.  Every chunk starts on a 4 KiB boundary
+ * (chunks sit align_up(chunk_size, 4096) bytes apart), so direct file reads
+ * can land in them.  Allocation is slow (pages are pinned); do it once,
+ * outside the load path.
+ * Errors: INVAL, HIP (pinned allocation failed). */
+int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int32_t device,
+                         sllm_pool** out);
+
+/* Free the pool.  BUSY while an open checkpoint handle still uses it. */
+int32_t sllm_pool_destroy(sllm_pool* pool);
+
+typedef struct sllm_pool_info {
+    uint64_t chunk_size;
+    uint64_t n_chunks;
+    uint64_t free_chunks;
+    uint64_t cached_checkpoints;
+} sllm_pool_info;
+int32_t sllm_pool_query(const sllm_pool* pool, sllm_pool_info* out);
+
+/* Read the whole partition of checkpoint directory `dir` into pool chunks,
+ * where it stays (cached in DRAM) until sllm_pool_evict.  Loads of handles
+ * opened on this pool then copy from these chunks with no file I/O.
+ * io_threads = 0 means 4.  flags: SLLM_OPEN_DIRECT_IO.
+ * Errors: INVAL, IO, FORMAT, NOMEM (not enough free chunks), BUSY (already
+ * cached).  The checkpoint is identified by the data file's device, inode,
+ * size and modification time. */
+int32_t sllm_pool_cache(sllm_pool* pool, const char* dir, uint32_t io_threads,
+                        uint32_t flags);
+
+/* Return a cached checkpoint's chunks to the pool.  NOTFOUND if not cached,
+ * BUSY while an open handle loads from it. */
+int32_t sllm_pool_evict(sllm_pool* pool, const char* dir);
+
+/* =========================================================================
+ * Open / load / index (Sec. 4.1 direct tensor addressing; Sec. 4.2 loading)
+ * ========================================================================= */
+
+#define SLLM_ENGINE_KERNEL 0u   /* gfx950 kernel reads mapped host chunks      */
+#define SLLM_ENGINE_SDMA   1u   /* hipMemcpyAsync on the copy engines          */
+
+#define SLLM_OPEN_DIRECT_IO 1u  /* O_DIRECT file reads (buffered if the file
+                                   system refuses them; see stats.direct_io) */
+#define SLLM_OPEN_TIMING    2u  /* time device work with HIP events (stats)   */
+
+typedef struct sllm_open_opts {
+    uint64_t   chunk_size;     /* C for reads from the file; 0 = pool's chunk
+                                  size if a pool is given, else the index's */
+    uint64_t   dev_alignment;  /* 0: device layout = file layout.  Else A2, a
+                                  power of two >= 16: tensor i goes to
+                                  d_i = sum_{j<i} align_up(s_j, A2), zero
+                                  padded, T2 = sum align_up(s_i, A2) bytes */
+    sllm_pool* pool;           /* NULL: a private pool of ring_slots chunks
+                                  is allocated by sllm_open                 */
+    uint32_t   io_threads;     /* file-reading threads; 0 = 4               */
+    uint32_t   n_streams;      /* copy streams for the SDMA engine; 0 = 2   */
+    uint32_t   ring_slots;     /* chunks in flight when streaming from the
+                                  file; 0 = 2 * io_threads                  */
+    uint32_t   engine;         /* SLLM_ENGINE_*                             */
+    uint32_t   flags;          /* SLLM_OPEN_*                               */
+    int32_t    device;         /* HIP device ordinal                        */
+} sllm_open_opts;
+
+typedef struct sllm_ckpt sllm_ckpt;
+
+/* Read and validate dir/sllm.index (magic, version, CRC, unique names,
+ * sizes = numel * itemsize, aligned ordered non-overlapping offsets,
+ * T = padded sum, file length F) and open dir/sllm.part0.  If `opts->pool`
+ * caches this checkpoint, later loads copy from the cached chunks; else they
+ * stream the file through ring_slots pool chunks.  opts may be NULL
+ * (defaults above, device 0).
+ * Errors: INVAL, IO, FORMAT, NOMEM, HIP. */
+int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out);
+
+/* Bytes a load writes: T (file layout) or T2 (dev_alignment != 0). */
+uint64_t sllm_total_bytes(const sllm_ckpt* h);
+
+/* Load the checkpoint into device memory [dev_dst, dev_dst + total_bytes).
+ * dev_dst must be 16-byte aligned.  All of [0, total) is written, padding
+ * included (as zero); bytes past it are untouched.  Returns once every file
+ * read has finished and every copy or kernel has been enqueued; completion is
+ * ordered on `stream`: work queued there after this call sees every byte.
+ * Errors: INVAL, RANGE (dst_bytes < total), IO, HIP, BUSY (another load on
+ * this handle).  On error, in-flight work is drained and the destination's
+ * contents are unspecified; the handle stays usable. */
+int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream);
+
+/* On-device repack of a file-layout image into the device layout: src holds
+ * the partition's first T bytes (as sllm_load writes them with
+ * dev_alignment = 0) and dst receives T2 bytes laid out with the handle's
+ * dev_alignment.  src and dst are device pointers, 16-byte aligned, and must
+ * not overlap.  Enqueued on `stream`.
+ * Errors: INVAL (handle opened without dev_alignment, overlap), RANGE, HIP. */
+int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes,
+                    void* dst_dev, uint64_t dst_bytes, void* stream);
+
+/* One tensor of the index.  `offset` is relative to the device buffer:
+ * the file offset o_i, or d_i when the handle has a dev_alignment.  `name`
+ * stays valid until sllm_close. */
+typedef struct sllm_tensor_info {
+    const char* name;
+    uint32_t    dtype;
+    uint32_t    ndim;
+    int64_t     shape[SLLM_MAX_NDIM];
+    uint64_t    offset;
+    uint64_t    nbytes;
+} sllm_tensor_info;
+
+/* Copy up to `cap` entries, in layout order, into out[] and set *n_total to
+ * the number of tensors (cap = 0 with out = NULL asks for the count only). */
+int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, uint64_t cap,
+                          uint64_t* n_total);
+
+/* Look one tensor up by name.  NOTFOUND if absent. */
+int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_tensor_info* out);
+
+typedef struct sllm_stats {
+    uint64_t bytes_loaded;      /* bytes written to the device by the last load  */
+    uint64_t bytes_read;        /* bytes read from the file by the last load     */
+    uint64_t n_chunks;          /* chunks moved by the last load                 */
+    uint64_t n_launches;        /* kernel launches or copy calls of the last load */
+    uint32_t engine;            /* engine used                                   */
+    uint32_t direct_io;         /* 1 if the file is read with O_DIRECT           */
+    uint32_t from_cache;        /* 1 if the last load came from cached chunks    */
+    uint32_t io_threads;
+    double   open_s;            /* wall time of sllm_open                        */
+    double   load_s;            /* wall time of the last sllm_load call          */
+    double   read_wait_s;       /* time the issue loop waited for file reads     */
+    double   device_ms;         /* device time of the last load (TIMING flag), else -1 */
+} sllm_stats;
+int32_t sllm_get_stats(const sllm_ckpt* h, sllm_stats* out);
+
+/* Close the handle; waits for its in-flight device work first. */
+int32_t sllm_close(sllm_ckpt* h);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* sllm_last_error(void);
+/* Static name of a status code. */
+const char* sllm_strerror(int32_t code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SLLM_H */

@@ -1,0 +1,332 @@
+"""ctypes binding of ``libsllm.so`` (the C ABI in ``include/sllm.h``).
+
+The raw entry points keep their C names (``sllm_convert``, ``sllm_open``,
+``sllm_load``, ``sllm_tensor_index`` ...) as attributes of :func:`lib`.  The
+helpers below only marshal arguments: every byte a load moves is moved by the
+library's HIP path.  torch is used for device memory, streams and the views
+over the loaded buffer.  If the library has not been built the helpers raise:
+there is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsllm.so")
+
+SLLM_OK = 0
+ERRORS = {-1: "SLLM_E_INVAL", -2: "SLLM_E_IO", -3: "SLLM_E_FORMAT", -4: "SLLM_E_NOMEM", -5: "SLLM_E_HIP",
+          -6: "SLLM_E_RANGE", -7: "SLLM_E_BUSY", -8: "SLLM_E_NOTFOUND"}
+DTYPE_CODE = {"f32": 0, "f16": 1, "bf16": 2, "i8": 3}
+CODE_DTYPE = {v: k for k, v in DTYPE_CODE.items()}
+ITEMSIZE = {0: 4, 1: 2, 2: 2, 3: 1}
+ENGINE = {"kernel": 0, "sdma": 1}
+OPEN_DIRECT_IO = 1
+OPEN_TIMING = 2
+CONVERT_FSYNC = 1
+MAX_NDIM = 8
+
+
+class SrcTensor(C.Structure):
+    _fields_ = [("name", C.c_char_p), ("dtype", C.c_uint32), ("ndim", C.c_uint32),
+                ("shape", C.POINTER(C.c_int64)), ("data", C.c_void_p), ("nbytes", C.c_uint64)]
+
+
+class ConvertOpts(C.Structure):
+    _fields_ = [("alignment", C.c_uint64), ("chunk_size", C.c_uint64), ("flags", C.c_uint32), ("reserved", C.c_uint32)]
+
+
+class PoolInfo(C.Structure):
+    _fields_ = [("chunk_size", C.c_uint64), ("n_chunks", C.c_uint64), ("free_chunks", C.c_uint64),
+                ("cached_checkpoints", C.c_uint64)]
+
+
+class OpenOpts(C.Structure):
+    _fields_ = [("chunk_size", C.c_uint64), ("dev_alignment", C.c_uint64), ("pool", C.c_void_p),
+                ("io_threads", C.c_uint32), ("n_streams", C.c_uint32), ("ring_slots", C.c_uint32),
+                ("engine", C.c_uint32), ("flags", C.c_uint32), ("device", C.c_int32)]
+
+
+class TensorInfo(C.Structure):
+    _fields_ = [("name", C.c_char_p), ("dtype", C.c_uint32), ("ndim", C.c_uint32),
+                ("shape", C.c_int64 * MAX_NDIM), ("offset", C.c_uint64), ("nbytes", C.c_uint64)]
+
+
+class Stats(C.Structure):
+    _fields_ = [("bytes_loaded", C.c_uint64), ("bytes_read", C.c_uint64), ("n_chunks", C.c_uint64),
+                ("n_launches", C.c_uint64), ("engine", C.c_uint32), ("direct_io", C.c_uint32),
+                ("from_cache", C.c_uint32), ("io_threads", C.c_uint32), ("open_s", C.c_double),
+                ("load_s", C.c_double), ("read_wait_s", C.c_double), ("device_ms", C.c_double)]
+
+
+# name -> (restype, argtypes); every symbol the header declares
+SIGNATURES = {
+    "sllm_convert": (C.c_int32, [C.POINTER(SrcTensor), C.c_uint64, C.c_char_p, C.POINTER(ConvertOpts)]),
+    "sllm_writer_open": (C.c_int32, [C.c_char_p, C.POINTER(ConvertOpts), C.POINTER(C.c_void_p)]),
+    "sllm_writer_add": (C.c_int32, [C.c_void_p, C.POINTER(SrcTensor)]),
+    "sllm_writer_close": (C.c_int32, [C.c_void_p]),
+    "sllm_writer_abort": (None, [C.c_void_p]),
+    "sllm_pool_create": (C.c_int32, [C.c_uint64, C.c_uint64, C.c_int32, C.POINTER(C.c_void_p)]),
+    "sllm_pool_destroy": (C.c_int32, [C.c_void_p]),
+    "sllm_pool_query": (C.c_int32, [C.c_void_p, C.POINTER(PoolInfo)]),
+    "sllm_pool_cache": (C.c_int32, [C.c_void_p, C.c_char_p, C.c_uint32, C.c_uint32]),
+    "sllm_pool_evict": (C.c_int32, [C.c_void_p, C.c_char_p]),
+    "sllm_open": (C.c_int32, [C.c_char_p, C.POINTER(OpenOpts), C.POINTER(C.c_void_p)]),
+    "sllm_total_bytes": (C.c_uint64, [C.c_void_p]),
+    "sllm_load": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p]),
+    "sllm_repack": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64, C.c_void_p]),
+    "sllm_tensor_index": (C.c_int32, [C.c_void_p, C.POINTER(TensorInfo), C.c_uint64, C.POINTER(C.c_uint64)]),
+    "sllm_tensor_find": (C.c_int32, [C.c_void_p, C.c_char_p, C.POINTER(TensorInfo)]),
+    "sllm_get_stats": (C.c_int32, [C.c_void_p, C.POINTER(Stats)]),
+    "sllm_close": (C.c_int32, [C.c_void_p]),
+    "sllm_last_error": (C.c_char_p, []),
+    "sllm_strerror": (C.c_char_p, [C.c_int32]),
+}
+
+_lib: Optional[C.CDLL] = None
+
+
+def lib() -> C.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with python -m paper_2401_14351_amd.build")
+        handle = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+class SllmError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {message}")
+        self.code = code
+        self.message = message
+
+
+def check(rc: int) -> None:
+    if rc != SLLM_OK:
+        raise SllmError(rc, lib().sllm_last_error().decode(errors="replace"))
+
+
+# ---------------------------------------------------------------------------
+# conversion
+# ---------------------------------------------------------------------------
+
+def _src_tensor(name: str, dtype: str, shape: Sequence[int], data) -> Tuple[SrcTensor, tuple]:
+    """Describe one tensor; returns the struct and the objects it points into."""
+    mv = memoryview(data).cast("B") if not hasattr(data, "data_ptr") else None
+    if mv is not None:
+        nbytes = mv.nbytes
+        ptr = C.addressof(C.c_char.from_buffer(mv)) if nbytes and not mv.readonly else None
+        keep: tuple = (mv,)
+        if nbytes and ptr is None:  # read-only buffer: borrow its address through a bytes copy
+            buf = C.create_string_buffer(mv.tobytes(), nbytes)
+            ptr, keep = C.addressof(buf), (buf,)
+    else:  # a contiguous CPU torch tensor
+        nbytes = data.numel() * data.element_size()
+        ptr, keep = data.data_ptr(), (data,)
+    shp = (C.c_int64 * max(1, len(shape)))(*[int(d) for d in shape])
+    raw = name.encode("utf-8")
+    st = SrcTensor(raw, DTYPE_CODE[dtype], len(shape), shp, ptr or None, nbytes)
+    return st, keep + (shp, raw)
+
+
+def convert(tensors: Iterable[Tuple[str, str, Sequence[int], object]], out_dir: str, alignment: int = 256,
+            chunk_size: int = 16 << 20, fsync: bool = False) -> None:
+    """``sllm_writer_*`` over an iterable of (name, dtype, shape, bytes-like).
+
+    Tensors are written as they arrive, so a generator never has to hold the
+    whole checkpoint in memory."""
+    L = lib()
+    opts = ConvertOpts(alignment, chunk_size, CONVERT_FSYNC if fsync else 0, 0)
+    w = C.c_void_p()
+    os.makedirs(out_dir, exist_ok=True)
+    check(L.sllm_writer_open(out_dir.encode(), C.byref(opts), C.byref(w)))
+    try:
+        for name, dtype, shape, data in tensors:
+            st, keep = _src_tensor(name, dtype, shape, data)
+            check(L.sllm_writer_add(w, C.byref(st)))
+            del keep
+    except BaseException:
+        L.sllm_writer_abort(w)
+        raise
+    check(L.sllm_writer_close(w))
+
+
+def convert_array(tensors: Sequence[Tuple[str, str, Sequence[int], object]], out_dir: str, alignment: int = 256,
+                  chunk_size: int = 16 << 20) -> None:
+    """``sllm_convert`` over a list held in memory."""
+    L = lib()
+    structs, keep = [], []
+    for t in tensors:
+        st, k = _src_tensor(*t)
+        structs.append(st)
+        keep.append(k)
+    arr = (SrcTensor * max(1, len(structs)))(*structs)
+    opts = ConvertOpts(alignment, chunk_size, 0, 0)
+    os.makedirs(out_dir, exist_ok=True)
+    check(L.sllm_convert(arr, len(structs), out_dir.encode(), C.byref(opts)))
+
+
+# ---------------------------------------------------------------------------
+# pool, open, load
+# ---------------------------------------------------------------------------
+
+def _stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        return None
+    return getattr(stream, "cuda_stream", stream)
+
+
+class Pool:
+    """The pinned host chunk pool (the DRAM tier)."""
+
+    def __init__(self, chunk_size: int, n_chunks: int, device: int = 0):
+        self._h = C.c_void_p()
+        check(lib().sllm_pool_create(chunk_size, n_chunks, device, C.byref(self._h)))
+        self.device = device
+
+    @property
+    def handle(self):
+        return self._h
+
+    def cache(self, ckpt_dir: str, io_threads: int = 4, direct_io: bool = False) -> None:
+        check(lib().sllm_pool_cache(self._h, ckpt_dir.encode(), io_threads, OPEN_DIRECT_IO if direct_io else 0))
+
+    def evict(self, ckpt_dir: str) -> None:
+        check(lib().sllm_pool_evict(self._h, ckpt_dir.encode()))
+
+    def info(self) -> Dict[str, int]:
+        inf = PoolInfo()
+        check(lib().sllm_pool_query(self._h, C.byref(inf)))
+        return {f: getattr(inf, f) for f, _ in PoolInfo._fields_}
+
+    def close(self) -> None:
+        if self._h:
+            check(lib().sllm_pool_destroy(self._h))
+            self._h = C.c_void_p()
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+@dataclass(frozen=True)
+class Tensor:
+    name: str
+    dtype: str
+    shape: Tuple[int, ...]
+    offset: int
+    nbytes: int
+
+
+class Checkpoint:
+    """An open converted checkpoint (``sllm_open`` ... ``sllm_close``)."""
+
+    def __init__(self, ckpt_dir: str, device: int = 0, pool: Optional[Pool] = None, chunk_size: int = 0,
+                 dev_alignment: int = 0, io_threads: int = 4, n_streams: int = 2, ring_slots: int = 0,
+                 engine: str = "kernel", direct_io: bool = False, timing: bool = False):
+        flags = (OPEN_DIRECT_IO if direct_io else 0) | (OPEN_TIMING if timing else 0)
+        opts = OpenOpts(chunk_size, dev_alignment, pool.handle if pool else None, io_threads, n_streams,
+                        ring_slots, ENGINE[engine], flags, device)
+        self._h = C.c_void_p()
+        check(lib().sllm_open(ckpt_dir.encode(), C.byref(opts), C.byref(self._h)))
+        self.device = device
+        self.dir = ckpt_dir
+
+    @property
+    def total_bytes(self) -> int:
+        return int(lib().sllm_total_bytes(self._h))
+
+    def tensors(self) -> List[Tensor]:
+        n = C.c_uint64()
+        check(lib().sllm_tensor_index(self._h, None, 0, C.byref(n)))
+        arr = (TensorInfo * max(1, n.value))()
+        check(lib().sllm_tensor_index(self._h, arr, n.value, C.byref(n)))
+        return [Tensor(t.name.decode(), CODE_DTYPE[t.dtype], tuple(t.shape[:t.ndim]), t.offset, t.nbytes)
+                for t in arr[:n.value]]
+
+    def find(self, name: str) -> Tensor:
+        t = TensorInfo()
+        check(lib().sllm_tensor_find(self._h, name.encode(), C.byref(t)))
+        return Tensor(t.name.decode(), CODE_DTYPE[t.dtype], tuple(t.shape[:t.ndim]), t.offset, t.nbytes)
+
+    def load(self, dst_ptr: int, dst_bytes: int, stream=None) -> None:
+        check(lib().sllm_load(self._h, dst_ptr, dst_bytes, _stream_ptr(stream)))
+
+    def load_into(self, buf, stream=None) -> None:
+        """Load into a uint8 torch tensor on the handle's device."""
+        self.load(buf.data_ptr(), buf.numel(), stream)
+
+    def repack(self, src, dst, stream=None) -> None:
+        check(lib().sllm_repack(self._h, src.data_ptr(), src.numel(), dst.data_ptr(), dst.numel(),
+                                _stream_ptr(stream)))
+
+    def stats(self) -> Dict[str, float]:
+        s = Stats()
+        check(lib().sllm_get_stats(self._h, C.byref(s)))
+        return {f: getattr(s, f) for f, _ in Stats._fields_}
+
+    def close(self) -> None:
+        if self._h:
+            check(lib().sllm_close(self._h))
+            self._h = C.c_void_p()
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def views(buf, tensors: Sequence[Tensor]) -> Dict[str, object]:
+    """torch views of each tensor at base + offset in ``buf`` (uint8).
+
+    A tensor whose offset is not a multiple of its element size (only in a
+    dense file layout, A < itemsize) is returned as its raw uint8 bytes."""
+    import torch
+
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8}
+    typed = {}
+    out = {}
+    for t in tensors:
+        isz = ITEMSIZE[DTYPE_CODE[t.dtype]]
+        if t.offset % isz:
+            out[t.name] = buf[t.offset:t.offset + t.nbytes]
+            continue
+        base = typed.get(t.dtype)
+        if base is None:
+            base = buf[: (buf.numel() // isz) * isz].view(tdt[t.dtype])
+            typed[t.dtype] = base
+        stride, acc = [], 1
+        for d in reversed(t.shape):
+            stride.append(acc)
+            acc *= max(int(d), 1)
+        out[t.name] = base.as_strided(t.shape, tuple(reversed(stride)), t.offset // isz)
+    return out
+
+
+def load(ckpt_dir: str, device: int = 0, stream=None, pool: Optional[Pool] = None, **opts):
+    """Open, load into a fresh uint8 device buffer, build views, synchronize.
+
+    Returns ``(buffer, {name: tensor view})``; the data are ready on return."""
+    import torch
+
+    with Checkpoint(ckpt_dir, device=device, pool=pool, **opts) as ck:
+        buf = torch.empty(max(ck.total_bytes, 1), dtype=torch.uint8, device=f"cuda:{device}")
+        s = stream if stream is not None else torch.cuda.current_stream(device)
+        ck.load_into(buf, s)
+        out = views(buf, ck.tensors())
+        s.synchronize()
+    return buf, out

@@ -1,0 +1,51 @@
+// Device layouts with their own alignment A2: tensor i of the partition goes
+// to d_i = sum_{j<i} align_up(s_j, A2) of the device buffer, zero padded (the
+// closed form of Sec. 4.1's aligned packing, applied with A2).
+//
+// The device keeps the index as three u64 tables (file offsets o, sizes s and
+// device offsets d, the last computed on the GPU by a wave64 prefix sum) and
+// a scatter kernel moves a window [x0, x1) of partition bytes to the device
+// bytes that window owns: the data bytes whose source lies in the window plus
+// the padding after every tensor whose last byte lies in it.  Windows that
+// tile [0, T) therefore write every byte of [0, T2) exactly once.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+#include <vector>
+
+namespace sllm {
+
+struct DeviceLayout {
+    uint64_t n = 0;                 // tensors
+    uint64_t total = 0;             // T: bytes of the partition image
+    uint64_t dev_total = 0;         // T2: bytes of the device image
+    uint64_t dev_align = 0;         // A2
+    uint64_t* d_off = nullptr;      // device: o_i
+    uint64_t* d_size = nullptr;     // device: s_i
+    uint64_t* d_dev = nullptr;      // device: d_i for i < n, d_n = T2
+    std::vector<uint64_t> h_off, h_dev, h_end;  // host: o_i, d_i, o_i + s_i
+    uint8_t* staging = nullptr;     // HBM staging chunks for copy-engine loads
+    uint64_t staging_stride = 0;
+};
+
+// Upload the tables, compute d on the device and check it against the host
+// plan `dev_off`/`dev_total`; allocate `staging_chunks` HBM chunks of `chunk`
+// bytes when asked.
+int32_t device_layout_build(const std::vector<uint64_t>& file_off, const std::vector<uint64_t>& sizes,
+                            const std::vector<uint64_t>& dev_off, uint64_t total, uint64_t dev_total,
+                            uint64_t dev_align, uint64_t staging_chunks, uint64_t chunk, DeviceLayout* out);
+void device_layout_free(DeviceLayout* l);
+
+// Move partition window [x0, x1), held contiguously at `src` (device memory,
+// or a device-visible mapping of pinned host memory), into the device image.
+int32_t launch_scatter_window(const DeviceLayout& l, uint8_t* dst, const uint8_t* src, uint64_t x0, uint64_t x1,
+                              bool src_is_host, hipStream_t stream);
+
+// Move the whole partition, held in pinned chunks listed by `table` (device
+// array; chunk k holds partition bytes [kC, kC + C)), into the device image.
+int32_t launch_scatter_table(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* table, uint64_t chunk,
+                             hipStream_t stream);
+
+}  // namespace sllm

@@ -1,0 +1,97 @@
+#include "io.hpp"
+
+#include <fcntl.h>
+#include <sys/stat.h>
+#include <sys/syscall.h>
+#include <unistd.h>
+
+#include <cerrno>
+#include <cstring>
+
+#include "common.hpp"
+
+#ifndef STATX_DIOALIGN
+#define STATX_DIOALIGN 0x00002000U
+#endif
+
+namespace sllm {
+
+namespace {
+
+// The O_DIRECT alignment the kernel reports for this file (statx with
+// STATX_DIOALIGN, Linux 6.1+), else the 4 KiB that common block devices
+// accept.  The two fields are read from the kernel's struct statx layout
+// (u32 stx_dio_mem_align at byte 152, u32 stx_dio_offset_align at 156) so
+// that older C library headers still build.
+uint64_t query_dio_align(int fd) {
+#ifdef SYS_statx
+    alignas(8) unsigned char sx[256];
+    std::memset(sx, 0, sizeof sx);
+    if (syscall(SYS_statx, fd, "", AT_EMPTY_PATH, STATX_DIOALIGN, sx) == 0) {
+        uint32_t mask, mem_align, off_align;
+        std::memcpy(&mask, sx + 0, 4);
+        std::memcpy(&mem_align, sx + 152, 4);
+        std::memcpy(&off_align, sx + 156, 4);
+        if ((mask & STATX_DIOALIGN) && off_align) return mem_align > off_align ? mem_align : off_align;
+    }
+#endif
+    return 4096;
+}
+
+}  // namespace
+
+int32_t open_data(const std::string& path, bool want_direct, DataFile* out) {
+    DataFile f;
+    if (want_direct) {
+        f.fd = ::open(path.c_str(), O_RDONLY | O_CLOEXEC | O_DIRECT);
+        if (f.fd >= 0) {
+            f.direct = true;
+        } else if (errno != EINVAL) {
+            return fail(SLLM_E_IO, "open %s: %s", path.c_str(), std::strerror(errno));
+        } else {
+            log_msg(1, "O_DIRECT refused for %s; reading buffered", path.c_str());
+        }
+    }
+    if (f.fd < 0) {
+        f.fd = ::open(path.c_str(), O_RDONLY | O_CLOEXEC);
+        if (f.fd < 0) return fail(SLLM_E_IO, "open %s: %s", path.c_str(), std::strerror(errno));
+    }
+    struct stat st;
+    if (::fstat(f.fd, &st) != 0) {
+        int32_t r = fail(SLLM_E_IO, "fstat %s: %s", path.c_str(), std::strerror(errno));
+        ::close(f.fd);
+        return r;
+    }
+    f.size = (uint64_t)st.st_size;
+    f.dev = (uint64_t)st.st_dev;
+    f.ino = (uint64_t)st.st_ino;
+    f.mtime_ns = (uint64_t)st.st_mtim.tv_sec * 1000000000ull + (uint64_t)st.st_mtim.tv_nsec;
+    f.dio_align = f.direct ? query_dio_align(f.fd) : 1;
+    *out = f;
+    return SLLM_OK;
+}
+
+void close_data(DataFile* f) {
+    if (f->fd >= 0) ::close(f->fd);
+    f->fd = -1;
+}
+
+int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const std::string& path) {
+    uint8_t* p = static_cast<uint8_t*>(buf);
+    while (n) {
+        ssize_t r = ::pread(f.fd, p, n, (off_t)off);
+        if (r < 0) {
+            if (errno == EINTR) continue;
+            return fail(SLLM_E_IO, "read %s at %llu: %s", path.c_str(), (unsigned long long)off, std::strerror(errno));
+        }
+        if (r == 0) return fail(SLLM_E_IO, "read %s at %llu: unexpected end of file", path.c_str(), (unsigned long long)off);
+        p += r;
+        off += (uint64_t)r;
+        n -= (uint64_t)r;
+    }
+    return SLLM_OK;
+}
+
+void drop_cache(const DataFile& f) { (void)::posix_fadvise(f.fd, 0, 0, POSIX_FADV_DONTNEED); }
+
+}  // namespace sllm

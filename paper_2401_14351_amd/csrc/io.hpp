@@ -1,0 +1,31 @@
+// File access for the storage tier (Sec. 4.2, "predictable data path"):
+// direct (O_DIRECT) reads into user buffers, with a labelled buffered
+// fallback where the file system refuses them.  Host-only (no HIP).
+#pragma once
+
+#include <cstdint>
+#include <string>
+
+namespace sllm {
+
+struct DataFile {
+    int fd = -1;
+    bool direct = false;     // opened with O_DIRECT
+    uint64_t dio_align = 0;  // offset/length/buffer alignment O_DIRECT needs
+    uint64_t size = 0;
+    uint64_t dev = 0, ino = 0, mtime_ns = 0;
+};
+
+// Open `path` read-only; with want_direct, try O_DIRECT first and fall back
+// to buffered reads if the file system rejects it.
+int32_t open_data(const std::string& path, bool want_direct, DataFile* out);
+void close_data(DataFile* f);
+
+// Read exactly n bytes at `off` (retrying short reads and EINTR).  Bytes
+// past the end of the file are an error.
+int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const std::string& path);
+
+// Drop the file's pages from the page cache (for cold-read measurements).
+void drop_cache(const DataFile& f);
+
+}  // namespace sllm

@@ -1,0 +1,36 @@
+// Host-side launchers of the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+namespace sllm {
+
+// Chunk gather in the file layout: for every chunk k in
+// [first_chunk, first_chunk + n_chunks), copy bytes [kC, min(kC + C, T)) of
+// the partition from that chunk's mapped pinned slot into dst + kC.
+// Slots come from `table` (a device array of n_chunks device-visible host
+// addresses, indexed from first_chunk) or, when table is null, `single`
+// (n_chunks must then be 1).
+struct GatherLaunch {
+    uint8_t* dst = nullptr;                  // device base of the whole image
+    const uint8_t* const* table = nullptr;   // device memory
+    const uint8_t* single = nullptr;         // device-visible host address
+    uint64_t chunk = 0;                      // C
+    uint64_t total = 0;                      // T
+    uint64_t first_chunk = 0;
+    uint64_t n_chunks = 0;
+};
+int32_t launch_gather(const GatherLaunch& g, hipStream_t stream);
+
+// Kernel launch shape knobs (read once from the environment:
+// SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT).
+struct GatherShape {
+    uint32_t blocks;   // persistent grid size
+    uint32_t unroll;   // 16-byte vectors per lane per tile: 1, 2 or 4
+    bool nontemporal;  // streaming (non-temporal) loads and stores
+};
+GatherShape gather_shape();
+
+}  // namespace sllm

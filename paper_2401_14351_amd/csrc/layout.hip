@@ -1,0 +1,341 @@
+// gfx950 kernels for device layouts with alignment A2.
+//
+// K3  offsets scan: d = exclusive prefix sum of align_up(s_i, A2) over the
+//     tensor index, one workgroup of 16 wave64s: a shuffle scan inside each
+//     wave, the 16 wave totals combined through LDS, a running carry across
+//     blocks of 1024 tensors.
+// K2  index-driven scatter (HBM source) and K1-scatter (mapped pinned host
+//     source): destination-driven.  Each workgroup owns a 16 KiB tile of the
+//     device image, finds the tensors whose slots meet the tile (binary
+//     search of d), stages those index entries in LDS, and then every lane
+//     produces aligned 16-byte destination vectors: a straight 16-byte load
+//     when source and destination agree mod 16, two aligned loads and a byte
+//     funnel shift when they do not, zeros for padding.  Only vectors cut by
+//     the window's first or last destination byte are written byte by byte.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+
+#include "common.hpp"
+#include "device_layout.hpp"
+#include "hip_util.hpp"
+
+namespace sllm {
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kThreads = 256;
+constexpr uint32_t kUnroll = 4;
+constexpr uint64_t kTile = (uint64_t)kThreads * 16 * kUnroll;  // destination bytes per tile
+constexpr uint32_t kLdsEntries = 256;                          // index entries staged per tile
+
+// ---------------------------------------------------------------------------
+// K3
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t x, uint32_t d) {
+    const int lo = __shfl_up((int)(uint32_t)x, d, 64);
+    const int hi = __shfl_up((int)(uint32_t)(x >> 32), d, 64);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// inclusive scan across the 64 lanes of a wave
+__device__ __forceinline__ uint64_t wave_scan(uint64_t x, uint32_t lane) {
+#pragma unroll
+    for (uint32_t d = 1; d < 64; d <<= 1) {
+        const uint64_t y = shfl_up64(x, d);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+__global__ __launch_bounds__(1024) void k3_offsets_scan(const uint64_t* __restrict__ size, uint64_t n,
+                                                        uint64_t align, uint64_t* __restrict__ dev) {
+    __shared__ uint64_t wave_tot[16];
+    const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint64_t carry = 0;
+    for (uint64_t base = 0; base < n; base += 1024) {
+        const uint64_t i = base + threadIdx.x;
+        const uint64_t v = i < n ? (size[i] + align - 1) & ~(align - 1) : 0;
+        const uint64_t incl = wave_scan(v, lane);
+        if (lane == 63) wave_tot[wave] = incl;
+        __syncthreads();
+        if (wave == 0) {
+            uint64_t w = lane < 16 ? wave_tot[lane] : 0;
+            w = wave_scan(w, lane);
+            if (lane < 16) wave_tot[lane] = w;
+        }
+        __syncthreads();
+        const uint64_t before = carry + (wave ? wave_tot[wave - 1] : 0);
+        if (i < n) dev[i] = before + incl - v;
+        carry += wave_tot[15];
+        __syncthreads();  // wave_tot is rewritten by the next block
+    }
+    if (threadIdx.x == 0) dev[n] = carry;
+}
+
+// ---------------------------------------------------------------------------
+// K2 / K1-scatter
+// ---------------------------------------------------------------------------
+
+struct ScatterArgs {
+    uint8_t* dst;
+    const uint64_t* off;   // o_i
+    const uint64_t* size;  // s_i
+    const uint64_t* dev;   // d_i, d_n = T2
+    uint64_t n;
+    uint64_t y0, y1;       // destination bytes written by this launch
+    uint64_t tile0, n_tiles;
+    // source: a contiguous window ...
+    const uint8_t* base;   // partition byte x at base[x - x0]
+    uint64_t x0, x1;
+    // ... or a table of chunks
+    const uint8_t* const* table;  // partition byte x at table[x / chunk][x % chunk]
+    uint64_t chunk;
+    uint64_t total;        // T
+    uint32_t vec_ok;       // 16-byte aligned source vectors are addressable as such
+};
+
+struct Src {
+    const ScatterArgs& a;
+    __device__ __forceinline__ const uint8_t* at(uint64_t x) const {
+        if (a.table) {
+            const uint64_t k = x / a.chunk;
+            return a.table[k] + (x - k * a.chunk);
+        }
+        return a.base + (x - a.x0);
+    }
+    // can the 16-byte aligned vectors covering [x, x + len) be loaded whole?
+    __device__ __forceinline__ bool vectors_ok(uint64_t xa, uint64_t len) const {
+        if (!a.vec_ok) return false;
+        if (a.table) return xa + len <= a.total;
+        return xa >= a.x0 && xa + len <= a.x1;
+    }
+};
+
+__device__ __forceinline__ u32x4 ld16(const uint8_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// bytes [s, s + 16) of the 32 bytes lo:hi, for s in [0, 16)
+__device__ __forceinline__ u32x4 funnel(u32x4 lo, u32x4 hi, uint32_t s) {
+    const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    const uint32_t b = s & 3;
+    u32x4 r;
+    switch (s >> 2) {
+        case 0: r = u32x4{__builtin_amdgcn_alignbyte(w[1], w[0], b), __builtin_amdgcn_alignbyte(w[2], w[1], b),
+                          __builtin_amdgcn_alignbyte(w[3], w[2], b), __builtin_amdgcn_alignbyte(w[4], w[3], b)}; break;
+        case 1: r = u32x4{__builtin_amdgcn_alignbyte(w[2], w[1], b), __builtin_amdgcn_alignbyte(w[3], w[2], b),
+                          __builtin_amdgcn_alignbyte(w[4], w[3], b), __builtin_amdgcn_alignbyte(w[5], w[4], b)}; break;
+        case 2: r = u32x4{__builtin_amdgcn_alignbyte(w[3], w[2], b), __builtin_amdgcn_alignbyte(w[4], w[3], b),
+                          __builtin_amdgcn_alignbyte(w[5], w[4], b), __builtin_amdgcn_alignbyte(w[6], w[5], b)}; break;
+        default: r = u32x4{__builtin_amdgcn_alignbyte(w[4], w[3], b), __builtin_amdgcn_alignbyte(w[5], w[4], b),
+                           __builtin_amdgcn_alignbyte(w[6], w[5], b), __builtin_amdgcn_alignbyte(w[7], w[6], b)}; break;
+    }
+    return r;
+}
+
+// keep bytes [0, keep) of v, zero the rest
+__device__ __forceinline__ u32x4 keep_bytes(u32x4 v, uint32_t keep) {
+    uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (uint32_t j = 0; j < 4; ++j) {
+        const uint32_t lo = 4 * j;
+        if (keep <= lo) w[j] = 0;
+        else if (keep < lo + 4) w[j] &= (1u << (8 * (keep - lo))) - 1u;
+    }
+    return u32x4{w[0], w[1], w[2], w[3]};
+}
+
+__device__ __forceinline__ uint32_t byte_of(u32x4 v, uint32_t b) {
+    const uint32_t w = b < 4 ? v.x : b < 8 ? v.y : b < 12 ? v.z : v.w;
+    return (w >> (8 * (b & 3))) & 0xFF;
+}
+
+// largest m in [lo, hi] with d[m] <= y (d[lo] <= y holds)
+__device__ __forceinline__ uint64_t owner_global(const uint64_t* d, uint64_t lo, uint64_t hi, uint64_t y) {
+    while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (d[mid] <= y) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
+    __shared__ uint64_t s_dev[kLdsEntries], s_off[kLdsEntries], s_size[kLdsEntries];
+    __shared__ uint64_t s_lo, s_hi;
+    const Src src{a};
+    for (uint64_t t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
+        const uint64_t yt = (a.tile0 + t) * kTile;
+        const uint64_t lo = yt > a.y0 ? yt : a.y0;
+        const uint64_t hi = yt + kTile < a.y1 ? yt + kTile : a.y1;
+        if (threadIdx.x == 0) {
+            const uint64_t i_lo = owner_global(a.dev, 0, a.n - 1, lo);
+            s_lo = i_lo;
+            s_hi = owner_global(a.dev, i_lo, a.n - 1, hi - 1);
+        }
+        __syncthreads();
+        const uint64_t i_lo = s_lo, cnt = s_hi - s_lo + 1;
+        const bool staged = cnt <= kLdsEntries;
+        if (staged && threadIdx.x < cnt) {
+            s_dev[threadIdx.x] = a.dev[i_lo + threadIdx.x];
+            s_off[threadIdx.x] = a.off[i_lo + threadIdx.x];
+            s_size[threadIdx.x] = a.size[i_lo + threadIdx.x];
+        }
+        __syncthreads();
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; ++u) {
+            const uint64_t y = yt + ((uint64_t)u * kThreads + threadIdx.x) * 16;
+            if (y + 16 <= lo || y >= hi) continue;
+            uint64_t dm, om, sm;
+            if (cnt == 1) {
+                dm = s_dev[0]; om = s_off[0]; sm = s_size[0];
+            } else if (staged) {
+                uint32_t l = 0, h = (uint32_t)cnt - 1;
+                while (l < h) {
+                    const uint32_t mid = (l + h + 1) >> 1;
+                    if (s_dev[mid] <= y) l = mid;
+                    else h = mid - 1;
+                }
+                dm = s_dev[l]; om = s_off[l]; sm = s_size[l];
+            } else {
+                const uint64_t m = owner_global(a.dev, i_lo, i_lo + cnt - 1, y);
+                dm = a.dev[m]; om = a.off[m]; sm = a.size[m];
+            }
+            const uint64_t r = y - dm;                   // byte of the slot
+            const uint32_t dn = sm > r ? (sm - r < 16 ? (uint32_t)(sm - r) : 16u) : 0u;  // data bytes in vector
+            const uint64_t x = om + r;                   // source of the vector's first byte
+            const bool whole = y >= lo && y + 16 <= hi;  // vector entirely ours to write
+            u32x4 v = u32x4{0, 0, 0, 0};
+            if (dn) {
+                const uint64_t xa = x & ~15ull;
+                const uint32_t sh = (uint32_t)(x & 15);
+                const uint64_t need = sh + dn > 16 ? 32 : 16;  // aligned source bytes spanned
+                if (whole && src.vectors_ok(xa, need)) {
+                    const u32x4 v0 = ld16(src.at(xa));
+                    v = sh == 0 ? v0 : funnel(v0, need == 32 ? ld16(src.at(xa + 16)) : v0, sh);
+                    if (dn < 16) v = keep_bytes(v, dn);
+                } else {
+                    uint32_t w[4] = {0, 0, 0, 0};
+                    for (uint32_t b = 0; b < dn; ++b) {
+                        if (y + b < lo || y + b >= hi) continue;
+                        w[b >> 2] |= (uint32_t)*src.at(x + b) << (8 * (b & 3));
+                    }
+                    v = u32x4{w[0], w[1], w[2], w[3]};
+                }
+            }
+            if (whole) {
+                *reinterpret_cast<u32x4*>(a.dst + y) = v;
+            } else {
+                for (uint32_t b = 0; b < 16; ++b)
+                    if (y + b >= lo && y + b < hi) a.dst[y + b] = (uint8_t)byte_of(v, b);
+            }
+        }
+        __syncthreads();  // LDS entries are restaged for the next tile
+    }
+}
+
+uint32_t env_blocks(const char* name, uint32_t dflt) {
+    const char* s = std::getenv(name);
+    long v = s ? std::strtol(s, nullptr, 10) : 0;
+    return v > 0 ? (uint32_t)v : dflt;
+}
+
+// first device byte owned by partition byte x: the first tensor whose data
+// ends after x starts owning there (padding belongs to a tensor's last byte)
+uint64_t y_of(const DeviceLayout& l, uint64_t x) {
+    auto it = std::upper_bound(l.h_end.begin(), l.h_end.end(), x);
+    if (it == l.h_end.end()) return l.dev_total;
+    const size_t i = (size_t)(it - l.h_end.begin());
+    return l.h_dev[i] + (x > l.h_off[i] ? x - l.h_off[i] : 0);
+}
+
+int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream_t stream) {
+    a.off = l.d_off;
+    a.size = l.d_size;
+    a.dev = l.d_dev;
+    a.n = l.n;
+    a.total = l.total;
+    if (a.y0 >= a.y1 || l.n == 0) return SLLM_OK;
+    if (a.y1 > l.dev_total) return fail(SLLM_E_INVAL, "scatter: destination range past the image");
+    a.tile0 = a.y0 / kTile;
+    a.n_tiles = ceil_div(a.y1, kTile) - a.tile0;
+    // host sources are PCIe-latency bound like K1; HBM sources want a full chip
+    const uint32_t want = src_is_host ? env_blocks("SLLM_K1_BLOCKS", 256) : env_blocks("SLLM_K2_BLOCKS", 2048);
+    const uint32_t grid = (uint32_t)std::min<uint64_t>(a.n_tiles, want);
+    k_scatter<<<dim3(grid), dim3(kThreads), 0, stream>>>(a);
+    SLLM_HIP(hipGetLastError());
+    return SLLM_OK;
+}
+
+}  // namespace
+
+int32_t device_layout_build(const std::vector<uint64_t>& file_off, const std::vector<uint64_t>& sizes,
+                            const std::vector<uint64_t>& dev_off, uint64_t total, uint64_t dev_total,
+                            uint64_t dev_align, uint64_t staging_chunks, uint64_t chunk, DeviceLayout* out) {
+    DeviceLayout& l = *out;
+    l.n = sizes.size();
+    l.total = total;
+    l.dev_total = dev_total;
+    l.dev_align = dev_align;
+    l.h_off = file_off;
+    l.h_dev = dev_off;
+    l.h_end.resize(l.n);
+    for (uint64_t i = 0; i < l.n; ++i) l.h_end[i] = file_off[i] + sizes[i];
+    if (staging_chunks) {
+        if (!align_up(chunk, 256, &l.staging_stride)) return fail(SLLM_E_INVAL, "chunk size overflows");
+        SLLM_HIP(hipMalloc(reinterpret_cast<void**>(&l.staging), staging_chunks * l.staging_stride));
+    }
+    if (l.n == 0) return SLLM_OK;
+    const size_t bytes = l.n * sizeof(uint64_t);
+    SLLM_HIP(hipMalloc(reinterpret_cast<void**>(&l.d_off), bytes));
+    SLLM_HIP(hipMalloc(reinterpret_cast<void**>(&l.d_size), bytes));
+    SLLM_HIP(hipMalloc(reinterpret_cast<void**>(&l.d_dev), bytes + sizeof(uint64_t)));
+    SLLM_HIP(hipMemcpy(l.d_off, file_off.data(), bytes, hipMemcpyHostToDevice));
+    SLLM_HIP(hipMemcpy(l.d_size, sizes.data(), bytes, hipMemcpyHostToDevice));
+    k3_offsets_scan<<<dim3(1), dim3(1024), 0, nullptr>>>(l.d_size, l.n, dev_align, l.d_dev);
+    SLLM_HIP(hipGetLastError());
+    std::vector<uint64_t> got(l.n + 1);
+    SLLM_HIP(hipMemcpy(got.data(), l.d_dev, bytes + sizeof(uint64_t), hipMemcpyDeviceToHost));
+    for (uint64_t i = 0; i < l.n; ++i)
+        if (got[i] != dev_off[i])
+            return fail(SLLM_E_HIP, "device offsets scan disagrees at tensor %llu: %llu vs %llu", (unsigned long long)i,
+                        (unsigned long long)got[i], (unsigned long long)dev_off[i]);
+    if (got[l.n] != dev_total) return fail(SLLM_E_HIP, "device offsets scan total disagrees");
+    return SLLM_OK;
+}
+
+void device_layout_free(DeviceLayout* l) {
+    for (void* p : {(void*)l->d_off, (void*)l->d_size, (void*)l->d_dev, (void*)l->staging})
+        if (p) (void)hipFree(p);
+    *l = DeviceLayout{};
+}
+
+int32_t launch_scatter_window(const DeviceLayout& l, uint8_t* dst, const uint8_t* src, uint64_t x0, uint64_t x1,
+                              bool src_is_host, hipStream_t stream) {
+    ScatterArgs a{};
+    a.dst = dst;
+    a.base = src;
+    a.x0 = x0;
+    a.x1 = x1;
+    a.vec_ok = (reinterpret_cast<uintptr_t>(src) % 16 == 0) && (x0 % 16 == 0);
+    a.y0 = y_of(l, x0);
+    a.y1 = y_of(l, x1);
+    return launch(l, a, src_is_host, stream);
+}
+
+int32_t launch_scatter_table(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* table, uint64_t chunk,
+                             hipStream_t stream) {
+    ScatterArgs a{};
+    a.dst = dst;
+    a.table = table;
+    a.chunk = chunk;
+    a.vec_ok = chunk % 16 == 0;
+    a.y0 = 0;
+    a.y1 = l.dev_total;
+    return launch(l, a, /*src_is_host=*/true, stream);
+}
+
+}  // namespace sllm

@@ -1,0 +1,570 @@
+// Opening a converted checkpoint and loading it into one device buffer
+// (Sec. 4.1 direct tensor addressing; Sec. 4.2 multi-tier loading).
+//
+// Two sources feed a load:
+//  * cached: the partition already sits in pool chunks (the DRAM tier); the
+//    whole image moves in one K1 launch or in merged SDMA copies.
+//  * streamed: a task-queue pipeline.  I/O threads take the next chunk
+//    number, read that chunk from the file into a free pinned slot and queue
+//    (chunk, slot) for the issue loop, which moves it to the GPU on one of
+//    the copy streams and records the slot's completion event.  A slot is
+//    refilled only after its event has fired.
+#include <algorithm>
+#include <atomic>
+#include <condition_variable>
+#include <cstring>
+#include <deque>
+#include <mutex>
+#include <thread>
+#include <unordered_map>
+
+#include "device_layout.hpp"
+#include "hip_util.hpp"
+#include "kernels.hpp"
+#include "pool.hpp"
+
+using namespace sllm;
+
+namespace {
+
+struct Slot {
+    uint32_t id = 0;                  // pool chunk id
+    uint8_t* host = nullptr;
+    const uint8_t* mapped = nullptr;  // device-visible address of the same bytes
+    hipEvent_t done = nullptr;        // fires when the GPU no longer reads the slot
+    bool pending = false;
+};
+
+}  // namespace
+
+struct sllm_ckpt {
+    std::string dir, data_path;
+    IndexData ix;
+    std::unordered_map<std::string, uint32_t> by_name;
+    int device = 0;
+    uint64_t chunk = 0;             // C of this handle's loads
+    uint64_t dev_align = 0;         // A2, 0 for the file layout
+    std::vector<uint64_t> dev_off;  // offset of each tensor in the device buffer
+    uint64_t dev_total = 0;         // bytes a load writes (T or T2)
+    sllm_pool* pool = nullptr;
+    bool own_pool = false;
+    CacheEntry* cached = nullptr;
+    DataFile file;
+    uint32_t io_threads = 4, n_streams = 2, ring_slots = 8, engine = SLLM_ENGINE_KERNEL, flags = 0;
+    std::vector<Slot> slots;
+    std::vector<uint32_t> slot_ids;
+    std::vector<hipStream_t> streams;
+    std::vector<hipEvent_t> join_ev;
+    hipEvent_t fork_ev = nullptr, t0_ev = nullptr, t1_ev = nullptr;
+    bool timed = false;             // t0/t1 bracket the last load
+    DeviceLayout layout;            // device tables for A2 layouts
+    std::atomic<bool> busy{false};
+    sllm_stats stats{};
+};
+
+namespace {
+
+void release(sllm_ckpt* h) {
+    {
+        DeviceGuard guard(h->device);
+        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
+        for (Slot& s : h->slots)
+            if (s.done) {
+                if (s.pending) (void)hipEventSynchronize(s.done);
+                (void)hipEventDestroy(s.done);
+            }
+        for (hipEvent_t e : h->join_ev) (void)hipEventDestroy(e);
+        for (hipEvent_t e : {h->fork_ev, h->t0_ev, h->t1_ev})
+            if (e) (void)hipEventDestroy(e);
+        for (hipStream_t s : h->streams) (void)hipStreamDestroy(s);
+        device_layout_free(&h->layout);
+    }
+    if (h->pool) {
+        std::lock_guard<std::mutex> g(h->pool->mu);
+        if (!h->slot_ids.empty()) pool_give(h->pool, h->slot_ids);
+        if (h->cached) --h->cached->refs;
+        --h->pool->users;
+    }
+    if (h->own_pool) (void)sllm_pool_destroy(h->pool);
+    close_data(&h->file);
+    delete h;
+}
+
+// Make the copy streams wait for work already queued on `user`.
+int32_t fork_streams(sllm_ckpt* h, hipStream_t user) {
+    SLLM_HIP(hipEventRecord(h->fork_ev, user));
+    for (hipStream_t s : h->streams) SLLM_HIP(hipStreamWaitEvent(s, h->fork_ev, 0));
+    return SLLM_OK;
+}
+
+// Make `user` wait for everything queued on the copy streams.
+int32_t join_streams(sllm_ckpt* h, hipStream_t user) {
+    for (size_t i = 0; i < h->streams.size(); ++i) {
+        SLLM_HIP(hipEventRecord(h->join_ev[i], h->streams[i]));
+        SLLM_HIP(hipStreamWaitEvent(user, h->join_ev[i], 0));
+    }
+    return SLLM_OK;
+}
+
+uint64_t sdma_max_copy() {
+    static const uint64_t v = [] {
+        const char* s = std::getenv("SLLM_SDMA_MAX_COPY_MB");
+        long mb = s ? std::strtol(s, nullptr, 10) : 0;
+        return (mb > 0 ? (uint64_t)mb : 256ull) << 20;
+    }();
+    return v;
+}
+
+// Move one chunk (partition bytes [x0, x0 + len)) from a pinned slot to the
+// device on stream s, in the handle's device layout.
+int32_t move_chunk(sllm_ckpt* h, uint8_t* dst, uint64_t k, const uint8_t* host, const uint8_t* mapped, uint64_t len,
+                   uint32_t si, hipStream_t s) {
+    const uint64_t x0 = k * h->chunk;
+    if (h->dev_align) {
+        if (h->engine == SLLM_ENGINE_KERNEL)
+            return launch_scatter_window(h->layout, dst, mapped, x0, x0 + len, /*src_is_host=*/true, s);
+        // SDMA into this stream's HBM staging chunk, then repack on the same stream
+        uint8_t* stage = h->layout.staging + (uint64_t)si * h->layout.staging_stride;
+        SLLM_HIP(hipMemcpyAsync(stage, host, len, hipMemcpyHostToDevice, s));
+        return launch_scatter_window(h->layout, dst, stage, x0, x0 + len, /*src_is_host=*/false, s);
+    }
+    if (h->engine == SLLM_ENGINE_SDMA) {
+        SLLM_HIP(hipMemcpyAsync(dst + x0, host, len, hipMemcpyHostToDevice, s));
+        return SLLM_OK;
+    }
+    GatherLaunch g;
+    g.dst = dst;
+    g.single = mapped;
+    g.chunk = h->chunk;
+    g.total = h->ix.total;
+    g.first_chunk = k;
+    g.n_chunks = 1;
+    return launch_gather(g, s);
+}
+
+int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
+    CacheEntry* e = h->cached;
+    sllm_pool* p = h->pool;
+    const uint64_t C = h->chunk, T = h->ix.total, n = e->chunks.size();
+    h->stats.n_chunks = n;
+    h->stats.from_cache = 1;
+    if (h->engine == SLLM_ENGINE_KERNEL) {
+        h->stats.n_launches = 1;
+        if (h->dev_align) return launch_scatter_table(h->layout, dst, e->d_table, C, user);
+        GatherLaunch g;
+        g.dst = dst;
+        g.table = e->d_table;
+        g.chunk = C;
+        g.total = T;
+        g.first_chunk = 0;
+        g.n_chunks = n;
+        return launch_gather(g, user);
+    }
+    SLLM_TRY(fork_streams(h, user));
+    const uint64_t max_copy = std::max(sdma_max_copy(), C);
+    uint64_t issued = 0;
+    for (uint64_t k = 0; k < n;) {
+        // merge chunks that are adjacent in host memory into one copy
+        uint64_t j = k + 1;
+        while (j < n && p->stride == C && p->host[e->chunks[j]] == p->host[e->chunks[j - 1]] + C &&
+               (j + 1 - k) * C <= max_copy)
+            ++j;
+        const uint64_t x0 = k * C, x1 = std::min(j * C, T);
+        const uint32_t si = (uint32_t)(issued % h->streams.size());
+        if (h->dev_align) {
+            for (uint64_t q = k; q < j; ++q) {
+                const uint64_t a = q * C, b = std::min(a + C, T);
+                SLLM_TRY(move_chunk(h, dst, q, p->host[e->chunks[q]], p->mapped[e->chunks[q]], b - a,
+                                    (uint32_t)((issued + q - k) % h->streams.size()), h->streams[(issued + q - k) % h->streams.size()]));
+            }
+            issued += j - k;
+        } else {
+            SLLM_HIP(hipMemcpyAsync(dst + x0, p->host[e->chunks[k]], x1 - x0, hipMemcpyHostToDevice, h->streams[si]));
+            ++issued;
+        }
+        k = j;
+    }
+    h->stats.n_launches = issued;
+    return join_streams(h, user);
+}
+
+// The streamed pipeline: io_threads readers feed the issue loop through two queues.
+int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
+    const uint64_t C = h->chunk, T = h->ix.total;
+    const uint64_t n = ceil_div(T, C);
+    const uint64_t read_end = h->file.direct ? h->ix.file_bytes : T;
+    h->stats.n_chunks = n;
+    SLLM_TRY(fork_streams(h, user));
+
+    std::mutex mu;
+    std::condition_variable cv_free, cv_ready;
+    std::deque<uint32_t> free_q;
+    std::deque<std::pair<uint64_t, uint32_t>> ready_q;
+    for (uint32_t i = 0; i < h->slots.size(); ++i) free_q.push_back(i);
+    std::atomic<uint64_t> next{0};
+    bool stop = false;
+    int32_t err = SLLM_OK;
+    std::string err_msg;
+    uint64_t bytes_read = 0;
+
+    auto set_error = [&](int32_t st) {  // caller holds mu
+        if (err == SLLM_OK) {
+            err = st;
+            err_msg = sllm_last_error();
+        }
+        stop = true;
+        cv_free.notify_all();
+        cv_ready.notify_all();
+    };
+
+    auto reader = [&] {
+        (void)hipSetDevice(h->device);
+        for (;;) {
+            const uint64_t k = next.fetch_add(1);
+            if (k >= n) return;
+            uint32_t si;
+            {
+                std::unique_lock<std::mutex> lk(mu);
+                cv_free.wait(lk, [&] { return stop || !free_q.empty(); });
+                if (stop) return;
+                si = free_q.front();
+                free_q.pop_front();
+            }
+            Slot& s = h->slots[si];
+            int32_t st = SLLM_OK;
+            if (s.pending) {
+                hipError_t e = hipEventSynchronize(s.done);
+                if (e != hipSuccess) st = fail(SLLM_E_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
+                s.pending = false;
+            }
+            const uint64_t off = k * C, len = std::min(C, read_end - off);
+            if (st == SLLM_OK) st = pread_full(h->file, s.host, len, off, h->data_path);
+            std::lock_guard<std::mutex> g(mu);
+            if (st != SLLM_OK) {
+                free_q.push_back(si);
+                set_error(st);
+                return;
+            }
+            bytes_read += len;
+            ready_q.emplace_back(k, si);
+            cv_ready.notify_one();
+        }
+    };
+
+    const uint32_t nt = (uint32_t)std::min<uint64_t>(h->io_threads, n);
+    std::vector<std::thread> threads;
+    threads.reserve(nt);
+    for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader);
+
+    double wait_s = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        std::pair<uint64_t, uint32_t> item;
+        {
+            const double w0 = now_s();
+            std::unique_lock<std::mutex> lk(mu);
+            cv_ready.wait(lk, [&] { return stop || !ready_q.empty(); });
+            wait_s += now_s() - w0;
+            if (ready_q.empty()) break;  // stopped by a reader's error
+            item = ready_q.front();
+            ready_q.pop_front();
+        }
+        const uint64_t k = item.first;
+        Slot& s = h->slots[item.second];
+        const uint32_t si = (uint32_t)(i % h->streams.size());
+        hipStream_t st = h->streams[si];
+        int32_t rc = move_chunk(h, dst, k, s.host, s.mapped, std::min(C, T - k * C), si, st);
+        if (rc == SLLM_OK) {
+            hipError_t e = hipEventRecord(s.done, st);
+            if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+        }
+        std::lock_guard<std::mutex> g(mu);
+        if (rc != SLLM_OK) {
+            free_q.push_back(item.second);
+            set_error(rc);
+            break;
+        }
+        s.pending = true;
+        free_q.push_back(item.second);
+        cv_free.notify_one();
+    }
+    {
+        std::lock_guard<std::mutex> g(mu);
+        if (err != SLLM_OK) stop = true;
+        cv_free.notify_all();
+    }
+    for (auto& t : threads) t.join();
+    h->stats.read_wait_s = wait_s;
+    h->stats.bytes_read = bytes_read;
+    h->stats.n_launches = n;
+    if (err != SLLM_OK) {
+        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);  // drain in-flight copies
+        return fail(err, "%s", err_msg.c_str());
+    }
+    return join_streams(h, user);
+}
+
+}  // namespace
+
+extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out) {
+    clear_error();
+    const double t0 = now_s();
+    if (!dir || !out) return fail(SLLM_E_INVAL, "dir and out must be non-NULL");
+    *out = nullptr;
+    sllm_open_opts o{};
+    if (opts) o = *opts;
+    if (o.engine != SLLM_ENGINE_KERNEL && o.engine != SLLM_ENGINE_SDMA) return fail(SLLM_E_INVAL, "unknown engine %u", o.engine);
+    if (o.flags & ~(SLLM_OPEN_DIRECT_IO | SLLM_OPEN_TIMING)) return fail(SLLM_E_INVAL, "unknown flags 0x%x", o.flags);
+    if (o.dev_alignment && (!is_pow2(o.dev_alignment) || o.dev_alignment < 16))
+        return fail(SLLM_E_INVAL, "device alignment %llu is not a power of two >= 16", (unsigned long long)o.dev_alignment);
+    if (o.pool && o.pool->device != o.device)
+        return fail(SLLM_E_INVAL, "pool belongs to device %d, not %d", o.pool->device, o.device);
+
+    auto* h = new (std::nothrow) sllm_ckpt;
+    if (!h) return fail(SLLM_E_NOMEM, "out of host memory");
+    h->dir = dir;
+    h->data_path = std::string(dir) + "/" + kDataName;
+    h->device = o.device;
+    h->io_threads = o.io_threads ? o.io_threads : 4;
+    h->n_streams = o.n_streams ? o.n_streams : 2;
+    h->ring_slots = o.ring_slots ? o.ring_slots : 2 * h->io_threads;
+    h->engine = o.engine;
+    h->flags = o.flags;
+    h->dev_align = o.dev_alignment;
+    auto bail = [&](int32_t st) {
+        std::string msg = sllm_last_error();
+        release(h);
+        return fail(st, "%s", msg.c_str());
+    };
+
+    std::string blob;
+    int32_t st = read_small_file(std::string(dir) + "/" + kIndexName, &blob);
+    if (st == SLLM_OK) st = decode_index(blob.data(), blob.size(), &h->ix);
+    if (st == SLLM_OK) st = open_data(h->data_path, (o.flags & SLLM_OPEN_DIRECT_IO) != 0, &h->file);
+    if (st != SLLM_OK) return bail(st);
+    if (h->file.size != h->ix.file_bytes) {
+        fail(SLLM_E_FORMAT, "%s is %llu bytes, the index says %llu", h->data_path.c_str(),
+             (unsigned long long)h->file.size, (unsigned long long)h->ix.file_bytes);
+        return bail(SLLM_E_FORMAT);
+    }
+    h->by_name.reserve(h->ix.tensors.size() * 2);
+    for (uint32_t i = 0; i < h->ix.tensors.size(); ++i) h->by_name.emplace(h->ix.tensors[i].name, i);
+
+    // device layout: the file offsets, or the closed form at A2
+    const size_t nt = h->ix.tensors.size();
+    h->dev_off.resize(nt);
+    if (h->dev_align) {
+        std::vector<uint64_t> sizes(nt);
+        for (size_t i = 0; i < nt; ++i) sizes[i] = h->ix.tensors[i].nbytes;
+        st = plan_layout(sizes.data(), nt, h->dev_align, h->dev_off.data(), &h->dev_total);
+        if (st != SLLM_OK) return bail(st);
+    } else {
+        for (size_t i = 0; i < nt; ++i) h->dev_off[i] = h->ix.tensors[i].offset;
+        h->dev_total = h->ix.total;
+    }
+
+    // the chunk pool: a shared one (maybe caching this partition) or a private ring
+    if (o.pool) {
+        h->pool = o.pool;
+        {
+            std::lock_guard<std::mutex> g(h->pool->mu);
+            ++h->pool->users;
+            h->cached = pool_find(h->pool, h->file);
+            if (h->cached) ++h->cached->refs;
+            h->chunk = h->cached ? h->pool->chunk : (o.chunk_size ? o.chunk_size : h->pool->chunk);
+            if (h->cached && o.chunk_size && o.chunk_size != h->pool->chunk)
+                st = fail(SLLM_E_INVAL, "cached partition uses the pool's chunk size %llu", (unsigned long long)h->pool->chunk);
+            else if (h->chunk > h->pool->chunk)
+                st = fail(SLLM_E_INVAL, "chunk size %llu exceeds the pool's %llu", (unsigned long long)h->chunk,
+                          (unsigned long long)h->pool->chunk);
+            else if (!h->cached)
+                st = pool_take(h->pool, h->ring_slots, &h->slot_ids);
+        }
+        if (st != SLLM_OK) return bail(st);
+    } else {
+        h->chunk = o.chunk_size ? o.chunk_size : h->ix.chunk_size;
+        st = sllm_pool_create(h->chunk, h->ring_slots, h->device, &h->pool);
+        if (st != SLLM_OK) return bail(st);
+        h->own_pool = true;
+        {
+            std::lock_guard<std::mutex> g(h->pool->mu);
+            ++h->pool->users;
+            st = pool_take(h->pool, h->ring_slots, &h->slot_ids);
+        }
+        if (st != SLLM_OK) return bail(st);
+    }
+    if (!h->cached && h->file.direct && h->chunk % h->file.dio_align) {
+        fail(SLLM_E_INVAL, "direct reads need chunk size %llu to be a multiple of %llu", (unsigned long long)h->chunk,
+             (unsigned long long)h->file.dio_align);
+        return bail(SLLM_E_INVAL);
+    }
+
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) {
+        fail(SLLM_E_HIP, "cannot make device %d current", h->device);
+        return bail(SLLM_E_HIP);
+    }
+    auto hip_ok = [&](hipError_t e, const char* what) {
+        if (e == hipSuccess) return true;
+        fail(SLLM_E_HIP, "%s failed: %s", what, hipGetErrorString(e));
+        return false;
+    };
+    h->streams.resize(h->n_streams, nullptr);
+    h->join_ev.resize(h->n_streams, nullptr);
+    for (uint32_t i = 0; i < h->n_streams; ++i) {
+        if (!hip_ok(hipStreamCreateWithFlags(&h->streams[i], hipStreamNonBlocking), "hipStreamCreateWithFlags") ||
+            !hip_ok(hipEventCreateWithFlags(&h->join_ev[i], hipEventDisableTiming), "hipEventCreateWithFlags"))
+            return bail(SLLM_E_HIP);
+    }
+    if (!hip_ok(hipEventCreateWithFlags(&h->fork_ev, hipEventDisableTiming), "hipEventCreateWithFlags") ||
+        !hip_ok(hipEventCreate(&h->t0_ev), "hipEventCreate") || !hip_ok(hipEventCreate(&h->t1_ev), "hipEventCreate"))
+        return bail(SLLM_E_HIP);
+    h->slots.resize(h->slot_ids.size());
+    for (size_t i = 0; i < h->slot_ids.size(); ++i) {
+        Slot& s = h->slots[i];
+        s.id = h->slot_ids[i];
+        s.host = h->pool->host[s.id];
+        s.mapped = h->pool->mapped[s.id];
+        if (!hip_ok(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreateWithFlags")) return bail(SLLM_E_HIP);
+    }
+    if (h->dev_align) {
+        std::vector<uint64_t> file_off(nt), sizes(nt);
+        for (size_t i = 0; i < nt; ++i) {
+            file_off[i] = h->ix.tensors[i].offset;
+            sizes[i] = h->ix.tensors[i].nbytes;
+        }
+        const uint64_t staging = (h->engine == SLLM_ENGINE_SDMA) ? h->n_streams : 0;
+        st = device_layout_build(file_off, sizes, h->dev_off, h->ix.total, h->dev_total, h->dev_align, staging,
+                                 h->chunk, &h->layout);
+        if (st != SLLM_OK) return bail(st);
+    }
+    h->stats.io_threads = h->io_threads;
+    h->stats.engine = h->engine;
+    h->stats.direct_io = h->file.direct ? 1 : 0;
+    h->stats.device_ms = -1;
+    h->stats.open_s = now_s() - t0;
+    *out = h;
+    return SLLM_OK;
+}
+
+extern "C" uint64_t sllm_total_bytes(const sllm_ckpt* h) { return h ? h->dev_total : 0; }
+
+extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream) {
+    clear_error();
+    if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
+    if (h->busy.exchange(true)) return fail(SLLM_E_BUSY, "a load is already running on this handle");
+    struct Unbusy {
+        std::atomic<bool>* b;
+        ~Unbusy() { b->store(false); }
+    } unbusy{&h->busy};
+    if (!dev_dst && h->dev_total) return fail(SLLM_E_INVAL, "destination is NULL");
+    if (reinterpret_cast<uintptr_t>(dev_dst) % 16) return fail(SLLM_E_INVAL, "destination is not 16-byte aligned");
+    if (dst_bytes < h->dev_total)
+        return fail(SLLM_E_RANGE, "destination holds %llu bytes, the checkpoint needs %llu", (unsigned long long)dst_bytes,
+                    (unsigned long long)h->dev_total);
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return fail(SLLM_E_HIP, "cannot make device %d current", h->device);
+    hipStream_t user = static_cast<hipStream_t>(stream);
+    const double t0 = now_s();
+    h->stats.bytes_loaded = 0;
+    h->stats.bytes_read = 0;
+    h->stats.n_chunks = 0;
+    h->stats.n_launches = 0;
+    h->stats.from_cache = 0;
+    h->stats.read_wait_s = 0;
+    h->stats.device_ms = -1;
+    h->timed = false;
+    const bool timing = (h->flags & SLLM_OPEN_TIMING) != 0;
+    if (timing) SLLM_HIP(hipEventRecord(h->t0_ev, user));
+    int32_t st = SLLM_OK;
+    if (h->dev_total) {
+        uint8_t* dst = static_cast<uint8_t*>(dev_dst);
+        st = h->cached ? load_cached(h, dst, user) : load_streamed(h, dst, user);
+    }
+    if (st != SLLM_OK) return st;
+    if (timing) {
+        SLLM_HIP(hipEventRecord(h->t1_ev, user));
+        h->timed = true;
+    }
+    h->stats.bytes_loaded = h->dev_total;
+    h->stats.load_s = now_s() - t0;
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes, void* dst_dev,
+                               uint64_t dst_bytes, void* stream) {
+    clear_error();
+    if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
+    if (!h->dev_align) return fail(SLLM_E_INVAL, "the handle was opened without a device alignment");
+    if (src_bytes < h->ix.total || dst_bytes < h->dev_total)
+        return fail(SLLM_E_RANGE, "repack needs %llu source and %llu destination bytes", (unsigned long long)h->ix.total,
+                    (unsigned long long)h->dev_total);
+    if ((reinterpret_cast<uintptr_t>(src_dev) | reinterpret_cast<uintptr_t>(dst_dev)) % 16)
+        return fail(SLLM_E_INVAL, "buffers must be 16-byte aligned");
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src_dev), d0 = reinterpret_cast<uintptr_t>(dst_dev);
+    if (h->ix.total && h->dev_total && s0 < d0 + h->dev_total && d0 < s0 + h->ix.total)
+        return fail(SLLM_E_INVAL, "source and destination overlap");
+    if (!h->dev_total) return SLLM_OK;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return fail(SLLM_E_HIP, "cannot make device %d current", h->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t* dst = static_cast<uint8_t*>(dst_dev);
+    return launch_scatter_window(h->layout, dst, static_cast<const uint8_t*>(src_dev), 0, h->ix.total,
+                                 /*src_is_host=*/false, s);
+}
+
+namespace {
+
+void fill_info(const sllm_ckpt* h, uint32_t i, sllm_tensor_info* out) {
+    const TensorRec& t = h->ix.tensors[i];
+    std::memset(out, 0, sizeof *out);
+    out->name = t.name.c_str();
+    out->dtype = t.dtype;
+    out->ndim = t.ndim;
+    for (uint32_t d = 0; d < t.ndim; ++d) out->shape[d] = t.shape[d];
+    out->offset = h->dev_off[i];
+    out->nbytes = t.nbytes;
+}
+
+}  // namespace
+
+extern "C" int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, uint64_t cap, uint64_t* n_total) {
+    clear_error();
+    if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
+    if (cap && !out) return fail(SLLM_E_INVAL, "out is NULL");
+    const uint64_t n = h->ix.tensors.size();
+    if (n_total) *n_total = n;
+    for (uint64_t i = 0; i < std::min(cap, n); ++i) fill_info(h, (uint32_t)i, &out[i]);
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_tensor_info* out) {
+    clear_error();
+    if (!h || !name || !out) return fail(SLLM_E_INVAL, "handle, name and out must be non-NULL");
+    auto it = h->by_name.find(name);
+    if (it == h->by_name.end()) return fail(SLLM_E_NOTFOUND, "no tensor named '%s'", name);
+    fill_info(h, it->second, out);
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_get_stats(const sllm_ckpt* hc, sllm_stats* out) {
+    clear_error();
+    if (!hc || !out) return fail(SLLM_E_INVAL, "handle and out must be non-NULL");
+    auto* h = const_cast<sllm_ckpt*>(hc);
+    if (h->timed) {
+        DeviceGuard guard(h->device);
+        float ms = 0;
+        SLLM_HIP(hipEventSynchronize(h->t1_ev));
+        SLLM_HIP(hipEventElapsedTime(&ms, h->t0_ev, h->t1_ev));
+        h->stats.device_ms = ms;
+    }
+    *out = h->stats;
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_close(sllm_ckpt* h) {
+    clear_error();
+    if (!h) return SLLM_OK;
+    if (h->busy.load()) return fail(SLLM_E_BUSY, "a load is running on this handle");
+    release(h);
+    return SLLM_OK;
+}

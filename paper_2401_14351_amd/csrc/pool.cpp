@@ -1,0 +1,302 @@
+// Pinned host chunk pool (the DRAM tier of Sec. 4.2) and the partitions
+// cached in it.
+#include "pool.hpp"
+
+#include <fcntl.h>
+#include <limits.h>
+#include <sys/stat.h>
+#include <unistd.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cerrno>
+#include <cstdlib>
+#include <cstring>
+#include <functional>
+#include <thread>
+
+#include "hip_util.hpp"
+
+using namespace sllm;
+
+namespace sllm {
+
+int32_t pool_take(sllm_pool* p, uint64_t n, std::vector<uint32_t>* out) {
+    if (n > p->free_ids.size())
+        return fail(SLLM_E_NOMEM, "pool has %zu free chunks, %llu needed", p->free_ids.size(), (unsigned long long)n);
+    out->clear();
+    out->reserve(n);
+    for (uint64_t i = 0; i < n; ++i) {
+        out->push_back(p->free_ids.back());
+        p->free_ids.pop_back();
+    }
+    return SLLM_OK;
+}
+
+void pool_give(sllm_pool* p, const std::vector<uint32_t>& ids) {
+    p->free_ids.insert(p->free_ids.end(), ids.begin(), ids.end());
+    // keep the lowest ids at the back so later takes get address-ordered runs
+    std::sort(p->free_ids.begin(), p->free_ids.end(), std::greater<uint32_t>());
+}
+
+CacheEntry* pool_find(sllm_pool* p, const DataFile& f) {
+    for (auto& e : p->cache)
+        if (e->dev == f.dev && e->ino == f.ino && e->size == f.size && e->mtime_ns == f.mtime_ns) return e.get();
+    return nullptr;
+}
+
+// Read a whole file into a string.
+int32_t read_small_file(const std::string& path, std::string* out) {
+    int fd = ::open(path.c_str(), O_RDONLY | O_CLOEXEC);
+    if (fd < 0) return fail(SLLM_E_IO, "open %s: %s", path.c_str(), std::strerror(errno));
+    struct stat st;
+    if (::fstat(fd, &st) != 0) {
+        ::close(fd);
+        return fail(SLLM_E_IO, "fstat %s: %s", path.c_str(), std::strerror(errno));
+    }
+    if (st.st_size > (1ll << 32)) {
+        ::close(fd);
+        return fail(SLLM_E_FORMAT, "%s is implausibly large", path.c_str());
+    }
+    out->resize((size_t)st.st_size);
+    size_t got = 0;
+    while (got < out->size()) {
+        ssize_t r = ::read(fd, &(*out)[got], out->size() - got);
+        if (r < 0 && errno == EINTR) continue;
+        if (r <= 0) {
+            ::close(fd);
+            return fail(SLLM_E_IO, "read %s: %s", path.c_str(), r < 0 ? std::strerror(errno) : "short read");
+        }
+        got += (size_t)r;
+    }
+    ::close(fd);
+    return SLLM_OK;
+}
+
+// Run fn(k) for k in [0, n) on `threads` threads; stop at the first failure
+// and return its status (with its message re-recorded on the calling thread).
+int32_t parallel_chunks(uint64_t n, uint32_t threads, int device, const std::function<int32_t(uint64_t)>& fn) {
+    std::atomic<uint64_t> next{0};
+    std::atomic<int32_t> status{SLLM_OK};
+    std::mutex mu;
+    std::string msg;
+    auto worker = [&] {
+        if (device >= 0) (void)hipSetDevice(device);
+        for (;;) {
+            if (status.load() != SLLM_OK) return;
+            uint64_t k = next.fetch_add(1);
+            if (k >= n) return;
+            int32_t st = fn(k);
+            if (st != SLLM_OK) {
+                std::lock_guard<std::mutex> g(mu);
+                if (status.load() == SLLM_OK) {
+                    msg = sllm_last_error();
+                    status.store(st);
+                }
+                return;
+            }
+        }
+    };
+    uint32_t nt = (uint32_t)std::min<uint64_t>(threads ? threads : 1, n ? n : 1);
+    std::vector<std::thread> pool;
+    for (uint32_t i = 1; i < nt; ++i) pool.emplace_back(worker);
+    worker();
+    for (auto& t : pool) t.join();
+    if (status.load() != SLLM_OK) return fail(status.load(), "%s", msg.c_str());
+    return SLLM_OK;
+}
+
+}  // namespace sllm
+
+namespace {
+
+uint64_t arena_target_bytes() {
+    const char* s = std::getenv("SLLM_POOL_ARENA_MB");
+    long mb = s ? std::strtol(s, nullptr, 10) : 0;
+    return (mb > 0 ? (uint64_t)mb : 1024ull) << 20;
+}
+
+void destroy_pool(sllm_pool* p) {
+    for (auto& e : p->cache)
+        if (e->d_table) (void)hipFree(e->d_table);
+    for (void* a : p->arenas) (void)hipHostFree(a);
+    delete p;
+}
+
+std::string canonical(const char* dir) {
+    char buf[PATH_MAX];
+    return ::realpath(dir, buf) ? std::string(buf) : std::string(dir);
+}
+
+}  // namespace
+
+extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int32_t device, sllm_pool** out) {
+    clear_error();
+    if (!out) return fail(SLLM_E_INVAL, "out is NULL");
+    *out = nullptr;
+    if (chunk_size == 0 || n_chunks == 0) return fail(SLLM_E_INVAL, "chunk size and chunk count must be >= 1");
+    if (n_chunks > 0xFFFFFFFFull) return fail(SLLM_E_INVAL, "too many chunks");
+    uint64_t stride, total;
+    if (!align_up(chunk_size, 4096, &stride) || !mul_ok(stride, n_chunks, &total))
+        return fail(SLLM_E_INVAL, "pool size overflows");
+    int count = 0;
+    SLLM_HIP(hipGetDeviceCount(&count));
+    if (device < 0 || device >= count) return fail(SLLM_E_INVAL, "device %d not present (%d devices)", device, count);
+    DeviceGuard guard(device);
+    if (!guard.ok()) return fail(SLLM_E_HIP, "cannot make device %d current", device);
+    auto* p = new (std::nothrow) sllm_pool;
+    if (!p) return fail(SLLM_E_NOMEM, "out of host memory");
+    p->device = device;
+    p->chunk = chunk_size;
+    p->stride = stride;
+    const uint64_t per_arena = std::max<uint64_t>(1, arena_target_bytes() / stride);
+    p->host.reserve(n_chunks);
+    p->mapped.reserve(n_chunks);
+    for (uint64_t done = 0; done < n_chunks;) {
+        const uint64_t k = std::min(per_arena, n_chunks - done);
+        void* h = nullptr;
+        hipError_t e = hipHostMalloc(&h, k * stride, hipHostMallocDefault);
+        if (e != hipSuccess) {
+            destroy_pool(p);
+            return fail(SLLM_E_HIP, "hipHostMalloc(%llu bytes) failed: %s", (unsigned long long)(k * stride), hipGetErrorString(e));
+        }
+        p->arenas.push_back(h);
+        void* d = nullptr;
+        e = hipHostGetDevicePointer(&d, h, 0);
+        if (e != hipSuccess) {
+            destroy_pool(p);
+            return fail(SLLM_E_HIP, "hipHostGetDevicePointer failed: %s", hipGetErrorString(e));
+        }
+        for (uint64_t i = 0; i < k; ++i) {
+            p->host.push_back(static_cast<uint8_t*>(h) + i * stride);
+            p->mapped.push_back(static_cast<const uint8_t*>(d) + i * stride);
+        }
+        done += k;
+    }
+    p->free_ids.resize(n_chunks);
+    for (uint64_t i = 0; i < n_chunks; ++i) p->free_ids[i] = (uint32_t)(n_chunks - 1 - i);
+    *out = p;
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_pool_destroy(sllm_pool* p) {
+    clear_error();
+    if (!p) return SLLM_OK;
+    {
+        std::lock_guard<std::mutex> g(p->mu);
+        if (p->users) return fail(SLLM_E_BUSY, "pool still used by %d open handle(s)", p->users);
+    }
+    DeviceGuard guard(p->device);
+    destroy_pool(p);
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_pool_query(const sllm_pool* pc, sllm_pool_info* out) {
+    clear_error();
+    if (!pc || !out) return fail(SLLM_E_INVAL, "pool and out must be non-NULL");
+    auto* p = const_cast<sllm_pool*>(pc);
+    std::lock_guard<std::mutex> g(p->mu);
+    out->chunk_size = p->chunk;
+    out->n_chunks = p->host.size();
+    out->free_chunks = p->free_ids.size();
+    out->cached_checkpoints = p->cache.size();
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_threads, uint32_t flags) {
+    clear_error();
+    if (!p || !dir) return fail(SLLM_E_INVAL, "pool and dir must be non-NULL");
+    if (flags & ~SLLM_OPEN_DIRECT_IO) return fail(SLLM_E_INVAL, "unknown flags 0x%x", flags);
+    const std::string data_path = std::string(dir) + "/" + kDataName;
+    std::string blob;
+    IndexData ix;
+    SLLM_TRY(read_small_file(std::string(dir) + "/" + kIndexName, &blob));
+    SLLM_TRY(decode_index(blob.data(), blob.size(), &ix));
+    DataFile f;
+    SLLM_TRY(open_data(data_path, (flags & SLLM_OPEN_DIRECT_IO) != 0, &f));
+    struct Closer {
+        DataFile* f;
+        ~Closer() { close_data(f); }
+    } closer{&f};
+    if (f.size != ix.file_bytes)
+        return fail(SLLM_E_FORMAT, "%s is %llu bytes, the index says %llu", data_path.c_str(),
+                    (unsigned long long)f.size, (unsigned long long)ix.file_bytes);
+    const uint64_t C = p->chunk;
+    if (f.direct && (C % f.dio_align || ix.file_bytes % f.dio_align))
+        return fail(SLLM_E_INVAL, "direct reads need chunk size %llu to be a multiple of %llu", (unsigned long long)C,
+                    (unsigned long long)f.dio_align);
+    const uint64_t n = ceil_div(ix.total, C);
+    std::vector<uint32_t> ids;
+    {
+        std::lock_guard<std::mutex> g(p->mu);
+        if (pool_find(p, f)) return fail(SLLM_E_BUSY, "%s is already cached", dir);
+        SLLM_TRY(pool_take(p, n, &ids));
+    }
+    auto give_back = [&] {
+        std::lock_guard<std::mutex> g(p->mu);
+        pool_give(p, ids);
+    };
+    // read chunk k into its pool chunk; direct reads run to the 4 KiB-padded
+    // file end so that their lengths stay block multiples
+    const uint64_t read_end = f.direct ? ix.file_bytes : ix.total;
+    int32_t st = parallel_chunks(n, io_threads ? io_threads : 4, -1, [&](uint64_t k) {
+        const uint64_t off = k * C;
+        return pread_full(f, p->host[ids[k]], std::min(C, read_end - off), off, data_path);
+    });
+    if (st != SLLM_OK) {
+        give_back();
+        return st;
+    }
+    auto e = std::make_unique<CacheEntry>();
+    e->dir = canonical(dir);
+    e->dev = f.dev;
+    e->ino = f.ino;
+    e->size = f.size;
+    e->mtime_ns = f.mtime_ns;
+    e->total = ix.total;
+    e->chunks = ids;
+    if (n) {
+        DeviceGuard guard(p->device);
+        std::vector<const uint8_t*> table(n);
+        for (uint64_t k = 0; k < n; ++k) table[k] = p->mapped[ids[k]];
+        hipError_t he = hipMalloc(reinterpret_cast<void**>(&e->d_table), n * sizeof(void*));
+        if (he == hipSuccess) he = hipMemcpy(e->d_table, table.data(), n * sizeof(void*), hipMemcpyHostToDevice);
+        if (he != hipSuccess) {
+            if (e->d_table) (void)hipFree(e->d_table);
+            give_back();
+            return fail(SLLM_E_HIP, "chunk table upload failed: %s", hipGetErrorString(he));
+        }
+    }
+    std::lock_guard<std::mutex> g(p->mu);
+    if (pool_find(p, f)) {  // cached concurrently by another thread
+        DeviceGuard guard(p->device);
+        if (e->d_table) (void)hipFree(e->d_table);
+        pool_give(p, ids);
+        return fail(SLLM_E_BUSY, "%s is already cached", dir);
+    }
+    p->cache.push_back(std::move(e));
+    return SLLM_OK;
+}
+
+extern "C" int32_t sllm_pool_evict(sllm_pool* p, const char* dir) {
+    clear_error();
+    if (!p || !dir) return fail(SLLM_E_INVAL, "pool and dir must be non-NULL");
+    const std::string canon = canonical(dir);
+    struct stat st;
+    const bool have = ::stat((std::string(dir) + "/" + kDataName).c_str(), &st) == 0;
+    std::lock_guard<std::mutex> g(p->mu);
+    for (size_t i = 0; i < p->cache.size(); ++i) {
+        CacheEntry& e = *p->cache[i];
+        const bool same = have ? (e.dev == (uint64_t)st.st_dev && e.ino == (uint64_t)st.st_ino) : e.dir == canon;
+        if (!same) continue;
+        if (e.refs) return fail(SLLM_E_BUSY, "%s is loaded by %d open handle(s)", dir, e.refs);
+        if (e.d_table) {
+            DeviceGuard guard(p->device);
+            (void)hipFree(e.d_table);
+        }
+        pool_give(p, e.chunks);
+        p->cache.erase(p->cache.begin() + (long)i);
+        return SLLM_OK;
+    }
+    return fail(SLLM_E_NOTFOUND, "%s is not cached", dir);
+}

@@ -1,0 +1,64 @@
+// Pinned host chunk pool: the DRAM tier of Sec. 4.2.  Fixed-size chunks avoid
+// fragmentation; the application allocates and frees them explicitly, and
+// whole partitions can stay cached in them between loads.
+#pragma once
+
+#include <cstdint>
+#include <functional>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "format.hpp"
+#include "io.hpp"
+
+namespace sllm {
+
+// A partition kept in pool chunks (chunk k of the partition in chunks[k]).
+struct CacheEntry {
+    std::string dir;
+    uint64_t dev = 0, ino = 0, size = 0, mtime_ns = 0;  // identity of the data file
+    uint64_t total = 0;                                 // T of the cached partition
+    std::vector<uint32_t> chunks;                       // pool chunk ids, partition order
+    const uint8_t** d_table = nullptr;                  // device array: mapped address of each chunk
+    int refs = 0;                                       // open handles that load from it
+};
+
+}  // namespace sllm
+
+struct sllm_pool {
+    int device = 0;
+    uint64_t chunk = 0;   // usable bytes per chunk
+    uint64_t stride = 0;  // distance between chunk starts: align_up(chunk, 4096)
+    std::vector<void*> arenas;            // pinned allocations
+    std::vector<uint8_t*> host;           // per chunk: host address
+    std::vector<const uint8_t*> mapped;   // per chunk: device-visible address
+    std::vector<uint32_t> free_ids;
+    std::vector<std::unique_ptr<sllm::CacheEntry>> cache;
+    int users = 0;                        // open handles attached to the pool
+    std::mutex mu;
+};
+
+namespace sllm {
+
+// Take n free chunks (NOMEM if fewer are free) / give them back.
+int32_t pool_take(sllm_pool* p, uint64_t n, std::vector<uint32_t>* out);
+void pool_give(sllm_pool* p, const std::vector<uint32_t>& ids);
+
+// The cache entry for this data file, or null (caller holds p->mu).
+CacheEntry* pool_find(sllm_pool* p, const DataFile& f);
+
+}  // namespace sllm
+
+namespace sllm {
+
+// Read a whole (small) file.
+int32_t read_small_file(const std::string& path, std::string* out);
+
+// Run fn(k) for every k in [0, n) on `threads` threads (the caller's among
+// them), stopping at the first failure; worker threads make `device`
+// current first when device >= 0.
+int32_t parallel_chunks(uint64_t n, uint32_t threads, int device, const std::function<int32_t(uint64_t)>& fn);
+
+}  // namespace sllm

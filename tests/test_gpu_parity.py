@@ -1,0 +1,315 @@
+"""GPU parity: every byte a load writes (padding included) equals the CPU
+oracle's image, for both engines, cached and streamed sources, the file
+layout and device layouts (A2), and every chunk size on tiny checkpoints.
+
+Expected bytes never come from the library: they are the oracle's partition
+image (or its A2 repack) built from the generator's tensor bytes."""
+
+import ctypes as C
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2401_14351_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = 0xA5
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    binding.lib()  # fail loudly if the library is missing
+    return torch
+
+
+def tensors_of(spec):
+    return [(t.name, t.dtype, t.shape, d) for t, d in zip(spec.tensors, synth.materialize(spec))]
+
+
+def expected(tensors, A, A2=0):
+    """The oracle's device image: the partition's first T bytes, or its A2 repack."""
+    index = oracle.make_index(tensors, A, 1)
+    H = oracle.partition_bytes(tensors, A)[:index.total_bytes]
+    if A2:
+        return bytes(oracle.repack(H, index, A2)), index
+    return bytes(H), index
+
+
+def run_load(torch, ck, expect_len, slack=64, stream=None):
+    buf = torch.full((expect_len + slack,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+    s = stream or torch.cuda.current_stream()
+    ck.load_into(buf, s)
+    s.synchronize()
+    host = buf.cpu().numpy()
+    assert (host[expect_len:] == SENTINEL).all(), "bytes past the image were written"
+    return host[:expect_len].tobytes()
+
+
+def assert_same(got, want, what):
+    if got != want:
+        a = np.frombuffer(got, np.uint8)
+        b = np.frombuffer(want, np.uint8)
+        bad = np.nonzero(a != b)[0]
+        raise AssertionError(f"{what}: {bad.size} bytes differ, first at {bad[:8].tolist()}")
+
+
+# ---------------------------------------------------------------------------
+# tiny checkpoints: every engine, source and layout
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("A", [1, 2, 16, 256, 4096])
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("A2", [0, 16, 256])
+def test_tiny_streamed(torch_cuda, tmp_path, A, engine, A2):
+    torch = torch_cuda
+    for seed in range(4):
+        spec = synth.tiny(seed, alignment=A, chunk_size=48)
+        tensors = tensors_of(spec)
+        binding.convert(iter(tensors), str(tmp_path / f"s{seed}"), A, spec.chunk_size)
+        want, _ = expected(tensors, A, A2)
+        say("tiny streamed", A, engine, A2, seed)
+        with binding.Checkpoint(str(tmp_path / f"s{seed}"), engine=engine, dev_alignment=A2, ring_slots=3,
+                                io_threads=2) as ck:
+            assert ck.total_bytes == len(want)
+            for rep in range(2):  # slots are reused across loads
+                assert_same(run_load(torch, ck, len(want)), want, f"seed {seed} rep {rep}")
+
+
+@pytest.mark.parametrize("A", [1, 16, 4096])
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("A2", [0, 32])
+def test_tiny_cached(torch_cuda, tmp_path, A, engine, A2):
+    torch = torch_cuda
+    for seed, C_ in ((0, 64), (1, 4096), (2, 100), (5, 16)):
+        spec = synth.tiny(seed, alignment=A)
+        tensors = tensors_of(spec)
+        d = str(tmp_path / f"c{seed}")
+        binding.convert(iter(tensors), d, A, C_)
+        want, index = expected(tensors, A, A2)
+        n_chunks = -(-index.total_bytes // C_) + 2
+        say("tiny cached", A, engine, A2, seed, C_)
+        with binding.Pool(C_, n_chunks) as pool:
+            pool.cache(d, io_threads=3)
+            with binding.Checkpoint(d, pool=pool, engine=engine, dev_alignment=A2) as ck:
+                assert ck.stats()["from_cache"] == 0
+                assert_same(run_load(torch, ck, len(want)), want, f"seed {seed}")
+                assert ck.stats()["from_cache"] == 1
+            pool.evict(d)
+            assert pool.info()["free_chunks"] == n_chunks
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("A,A2", [(16, 0), (1, 0), (4, 16)])
+def test_every_chunk_size(torch_cuda, tmp_path, engine, A, A2):
+    """Brute force over every chunk size that gives a distinct geometry."""
+    torch = torch_cuda
+    spec = synth.tiny(7, n=8, alignment=A, max_bytes=120)
+    tensors = tensors_of(spec)
+    d = str(tmp_path / "ck")
+    binding.convert(iter(tensors), d, A, 64)
+    want, index = expected(tensors, A, A2)
+    T = index.total_bytes
+    say("every chunk size", engine, A, A2, "T", T)
+    for C_ in list(range(1, T + 2)) + [index.file_bytes, index.file_bytes + 1]:
+        with binding.Checkpoint(d, engine=engine, chunk_size=C_, dev_alignment=A2, ring_slots=1 + C_ % 3,
+                                io_threads=1 + C_ % 2) as ck:
+            assert_same(run_load(torch, ck, len(want), slack=16), want, f"C={C_}")
+
+
+def test_empty_checkpoint(torch_cuda, tmp_path):
+    torch = torch_cuda
+    binding.convert([], str(tmp_path), 256, 4096)
+    with binding.Checkpoint(str(tmp_path)) as ck:
+        assert ck.total_bytes == 0 and ck.tensors() == []
+        run_load(torch, ck, 0)
+
+
+# ---------------------------------------------------------------------------
+# model-shaped workloads
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def opt125m(torch_cuda, tmp_path_factory):
+    spec = synth.opt_125m()
+    tensors = tensors_of(spec)
+    d = str(tmp_path_factory.mktemp("opt"))
+    binding.convert(iter(tensors), d, spec.alignment, spec.chunk_size)
+    return spec, tensors, d
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("cached", [True, False])
+def test_opt125m_file_layout(torch_cuda, opt125m, engine, cached):
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, index = expected(tensors, spec.alignment)
+    say("opt-125m", engine, "cached" if cached else "streamed")
+    pool = binding.Pool(spec.chunk_size, 32) if cached else None
+    try:
+        if pool:
+            pool.cache(d)
+        with binding.Checkpoint(d, pool=pool, engine=engine, timing=True) as ck:
+            got = run_load(torch, ck, len(want))
+            assert_same(got, want, "opt-125m")
+            st = ck.stats()
+            assert st["bytes_loaded"] == index.total_bytes and st["from_cache"] == int(cached)
+            assert st["device_ms"] > 0
+            # views at base + offset hold each tensor's bytes
+            buf = torch.empty(ck.total_bytes, dtype=torch.uint8, device="cuda:0")
+            ck.load_into(buf)
+            views = binding.views(buf, ck.tensors())
+            torch.cuda.synchronize()
+            for (name, dt, shape, data) in tensors[:40]:
+                v = views[name]
+                assert tuple(v.shape) == tuple(shape)
+                assert v.contiguous().view(torch.uint8).cpu().numpy().tobytes() == data.tobytes()
+    finally:
+        if pool:
+            pool.evict(d)
+            pool.close()
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine):
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    A2 = 4096
+    want2, _ = expected(tensors, spec.alignment, A2)
+    want1, _ = expected(tensors, spec.alignment)
+    say("opt-125m A2", engine)
+    with binding.Checkpoint(d, engine=engine, dev_alignment=A2) as ck:
+        assert_same(run_load(torch, ck, len(want2)), want2, "A2 load")
+        # the HBM-side repack (K2) of a file-layout image gives the same bytes
+        src = torch.frombuffer(bytearray(want1), dtype=torch.uint8).to("cuda:0")
+        dst = torch.full((len(want2) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+        ck.repack(src, dst)
+        torch.cuda.synchronize()
+        host = dst.cpu().numpy()
+        assert (host[len(want2):] == SENTINEL).all()
+        assert_same(host[:len(want2)].tobytes(), want2, "repack")
+
+
+def test_stress_prefix_device_layout(torch_cuda, tmp_path):
+    """Many small tensors of every dtype, 4 KiB file alignment, repacked to 256."""
+    torch = torch_cuda
+    spec = synth.stress(n=2000, max_bytes=1 << 18)
+    tensors = tensors_of(spec)
+    d = str(tmp_path)
+    binding.convert(iter(tensors), d, spec.alignment, spec.chunk_size)
+    for A2 in (0, 256, 16):
+        want, _ = expected(tensors, spec.alignment, A2)
+        for engine in ("kernel", "sdma"):
+            say("stress prefix", A2, engine)
+            with binding.Pool(spec.chunk_size, 1024) as pool:
+                pool.cache(d)
+                with binding.Checkpoint(d, pool=pool, engine=engine, dev_alignment=A2) as ck:
+                    assert_same(run_load(torch, ck, len(want)), want, f"cached A2={A2} {engine}")
+                pool.evict(d)
+            with binding.Checkpoint(d, engine=engine, dev_alignment=A2, chunk_size=1 << 20) as ck:
+                assert_same(run_load(torch, ck, len(want)), want, f"streamed A2={A2} {engine}")
+
+
+# ---------------------------------------------------------------------------
+# ordering and errors
+# ---------------------------------------------------------------------------
+
+def test_stream_ordering(torch_cuda, opt125m):
+    """Work queued before the load runs first; work queued after sees all bytes."""
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, _ = expected(tensors, spec.alignment)
+    s = torch.cuda.Stream()
+    with binding.Checkpoint(d, engine="sdma", n_streams=3) as ck:
+        buf = torch.empty(len(want), dtype=torch.uint8, device="cuda:0")
+        with torch.cuda.stream(s):
+            torch.cuda._sleep(20_000_000)   # keep the stream busy so ordering matters
+            buf.fill_(7)                    # queued before the load: must not clobber it
+        ck.load_into(buf, s)
+        with torch.cuda.stream(s):
+            checksum = buf[: 1 << 20].to(torch.int64).sum()
+        s.synchronize()
+        want_np = np.frombuffer(want, np.uint8)
+        assert int(checksum) == int(want_np[: 1 << 20].astype(np.int64).sum())
+        assert_same(buf.cpu().numpy().tobytes(), want, "ordered load")
+
+
+def test_load_errors(torch_cuda, opt125m):
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    with binding.Checkpoint(d) as ck:
+        small = torch.empty(ck.total_bytes - 1, dtype=torch.uint8, device="cuda:0")
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load_into(small)
+        assert ei.value.code == -6
+        buf = torch.empty(ck.total_bytes + 16, dtype=torch.uint8, device="cuda:0")
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load(buf.data_ptr() + 1, ck.total_bytes)
+        assert ei.value.code == -1
+        with pytest.raises(binding.SllmError) as ei:
+            ck.find("no.such.tensor")
+        assert ei.value.code == -8
+        # the handle still works after the errors
+        want, _ = expected(tensors, spec.alignment)
+        assert_same(run_load(torch, ck, len(want)), want, "after errors")
+
+
+def test_pool_rules(torch_cuda, opt125m):
+    spec, tensors, d = opt125m
+    with binding.Pool(spec.chunk_size, 4) as tiny_pool:
+        with pytest.raises(binding.SllmError) as ei:
+            tiny_pool.cache(d)             # 15 chunks needed
+        assert ei.value.code == -4
+        assert tiny_pool.info()["free_chunks"] == 4
+    pool = binding.Pool(spec.chunk_size, 20)
+    pool.cache(d)
+    with pytest.raises(binding.SllmError) as ei:
+        pool.cache(d)
+    assert ei.value.code == -7
+    ck = binding.Checkpoint(d, pool=pool)
+    with pytest.raises(binding.SllmError) as ei:
+        pool.evict(d)
+    assert ei.value.code == -7
+    with pytest.raises(binding.SllmError) as ei:
+        pool.close()
+    assert ei.value.code == -7
+    ck.close()
+    pool.evict(d)
+    with pytest.raises(binding.SllmError) as ei:
+        pool.evict(d)
+    assert ei.value.code == -8
+    pool.close()
+
+
+def test_io_error_mid_load(torch_cuda, tmp_path):
+    """A read failure stops the load with SLLM_E_IO; the handle stays usable."""
+    torch = torch_cuda
+    spec = synth.opt_125m()
+    tensors = tensors_of(spec)
+    d = tmp_path / "ck"
+    binding.convert(iter(tensors), str(d), spec.alignment, spec.chunk_size)
+    want, _ = expected(tensors, spec.alignment)
+    with binding.Checkpoint(str(d), chunk_size=1 << 20) as ck:
+        path = d / "sllm.part0"
+        full = open(path, "rb").read()
+        with open(path, "r+b") as f:
+            f.truncate(len(full) // 2)      # later chunks now hit end of file
+        buf = torch.empty(len(want), dtype=torch.uint8, device="cuda:0")
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load_into(buf)
+        assert ei.value.code == -2
+        with open(path, "wb") as f:
+            f.write(full)
+        assert_same(run_load(torch, ck, len(want)), want, "after restoring the file")
