@@ -245,6 +245,9 @@ typedef struct sllm_stats {
     double   load_s;            /* wall time of the last sllm_load call          */
     double   read_wait_s;       /* time the issue loop waited for file reads     */
     double   device_ms;         /* device time of the last load (TIMING flag), else -1 */
+    uint64_t bytes_bounced;     /* direct-read bytes staged through a bounce buffer
+                                   because the kernel refused direct transfers
+                                   into the pinned chunks                      */
 } sllm_stats;
 int32_t sllm_get_stats(const sllm_ckpt* h, sllm_stats* out);
 

@@ -60,7 +60,8 @@ class Stats(C.Structure):
     _fields_ = [("bytes_loaded", C.c_uint64), ("bytes_read", C.c_uint64), ("n_chunks", C.c_uint64),
                 ("n_launches", C.c_uint64), ("engine", C.c_uint32), ("direct_io", C.c_uint32),
                 ("from_cache", C.c_uint32), ("io_threads", C.c_uint32), ("open_s", C.c_double),
-                ("load_s", C.c_double), ("read_wait_s", C.c_double), ("device_ms", C.c_double)]
+                ("load_s", C.c_double), ("read_wait_s", C.c_double), ("device_ms", C.c_double),
+                ("bytes_bounced", C.c_uint64)]
 
 
 # name -> (restype, argtypes); every symbol the header declares
@@ -90,13 +91,40 @@ SIGNATURES = {
 _lib: Optional[C.CDLL] = None
 
 
+def _hip_runtimes() -> List[str]:
+    """Paths of the HIP runtime libraries mapped into this process."""
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                p = line.split()[-1]
+                if "libamdhip64" in os.path.basename(p):
+                    paths.add(os.path.realpath(p))
+    except OSError:
+        pass
+    return sorted(paths)
+
+
 def lib() -> C.CDLL:
-    """The loaded library (raises if it has not been built)."""
+    """The loaded library (raises if it has not been built).
+
+    torch ships its own HIP runtime under the same soname.  It is imported
+    first so that the library binds to that one runtime: stream handles and
+    device pointers from torch are only meaningful to the runtime that made
+    them, and a second runtime in the process finds no device."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with python -m paper_2401_14351_amd.build")
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         handle = C.CDLL(LIB_PATH)
+        runtimes = _hip_runtimes()
+        if len(runtimes) > 1:
+            raise RuntimeError(f"two HIP runtimes are loaded ({', '.join(runtimes)}); load torch before "
+                               f"{os.path.basename(LIB_PATH)}")
         for name, (res, args) in SIGNATURES.items():
             fn = getattr(handle, name)
             fn.restype = res

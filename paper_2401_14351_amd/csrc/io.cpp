@@ -6,6 +6,7 @@
 #include <unistd.h>
 
 #include <cerrno>
+#include <cstdlib>
 #include <cstring>
 
 #include "common.hpp"
@@ -76,19 +77,74 @@ void close_data(DataFile* f) {
     f->fd = -1;
 }
 
-int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const std::string& path) {
+namespace {
+
+// 0 on success, else the errno of the failing read (-1 for end of file).
+int pread_exact(int fd, void* buf, uint64_t n, uint64_t off) {
     uint8_t* p = static_cast<uint8_t*>(buf);
     while (n) {
-        ssize_t r = ::pread(f.fd, p, n, (off_t)off);
+        ssize_t r = ::pread(fd, p, n, (off_t)off);
         if (r < 0) {
             if (errno == EINTR) continue;
-            return fail(SLLM_E_IO, "read %s at %llu: %s", path.c_str(), (unsigned long long)off, std::strerror(errno));
+            return errno;
         }
-        if (r == 0) return fail(SLLM_E_IO, "read %s at %llu: unexpected end of file", path.c_str(), (unsigned long long)off);
+        if (r == 0) return -1;
         p += r;
         off += (uint64_t)r;
         n -= (uint64_t)r;
     }
+    return 0;
+}
+
+int32_t read_error(int e, const std::string& path, uint64_t off) {
+    if (e < 0) return fail(SLLM_E_IO, "read %s at %llu: unexpected end of file", path.c_str(), (unsigned long long)off);
+    return fail(SLLM_E_IO, "read %s at %llu: %s", path.c_str(), (unsigned long long)off, std::strerror(e));
+}
+
+constexpr uint64_t kBounceBytes = 4u << 20;
+
+struct Bounce {
+    void* p = nullptr;
+    ~Bounce() { std::free(p); }
+};
+
+uint8_t* bounce_buffer() {
+    thread_local Bounce b;
+    if (!b.p && posix_memalign(&b.p, 4096, kBounceBytes) != 0) b.p = nullptr;
+    return static_cast<uint8_t*>(b.p);
+}
+
+}  // namespace
+
+int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const std::string& path) {
+    int e = pread_exact(f.fd, buf, n, off);
+    return e ? read_error(e, path, off) : SLLM_OK;
+}
+
+int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
+                   uint64_t* bounced) {
+    if (!f.direct) return pread_full(f, dst, n, off, path);
+    if (f.direct_into_pinned->load() != 0) {
+        int e = pread_exact(f.fd, dst, n, off);
+        if (e == 0) {
+            f.direct_into_pinned->store(1);
+            return SLLM_OK;
+        }
+        if (e != EFAULT) return read_error(e, path, off);
+        if (f.direct_into_pinned->exchange(0) != 0)
+            log_msg(1, "direct reads cannot target pinned chunks; staging through a bounce buffer");
+    }
+    uint8_t* b = bounce_buffer();
+    if (!b) return fail(SLLM_E_NOMEM, "no memory for a direct-read bounce buffer");
+    uint8_t* d = static_cast<uint8_t*>(dst);
+    for (uint64_t done = 0; done < n;) {
+        const uint64_t k = n - done < kBounceBytes ? n - done : kBounceBytes;
+        int e = pread_exact(f.fd, b, k, off + done);
+        if (e) return read_error(e, path, off + done);
+        std::memcpy(d + done, b, k);
+        done += k;
+    }
+    if (bounced) *bounced += n;
     return SLLM_OK;
 }
 

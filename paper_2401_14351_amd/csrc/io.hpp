@@ -3,7 +3,9 @@
 // fallback where the file system refuses them.  Host-only (no HIP).
 #pragma once
 
+#include <atomic>
 #include <cstdint>
+#include <memory>
 #include <string>
 
 namespace sllm {
@@ -14,6 +16,9 @@ struct DataFile {
     uint64_t dio_align = 0;  // offset/length/buffer alignment O_DIRECT needs
     uint64_t size = 0;
     uint64_t dev = 0, ino = 0, mtime_ns = 0;
+    // whether direct reads may land in pinned chunks: -1 not yet known, 0 no
+    // (the kernel cannot pin those pages for the transfer), 1 yes
+    std::shared_ptr<std::atomic<int>> direct_into_pinned = std::make_shared<std::atomic<int>>(-1);
 };
 
 // Open `path` read-only; with want_direct, try O_DIRECT first and fall back
@@ -24,6 +29,13 @@ void close_data(DataFile* f);
 // Read exactly n bytes at `off` (retrying short reads and EINTR).  Bytes
 // past the end of the file are an error.
 int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const std::string& path);
+
+// Read one chunk into a pinned pool chunk.  With O_DIRECT the bytes go
+// straight into `dst`; where the kernel refuses direct transfers into that
+// memory (EFAULT: the pages cannot be pinned for I/O), they go through a
+// 4 MiB aligned per-thread bounce buffer instead, and *bounced counts them.
+int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
+                   uint64_t* bounced);
 
 // Drop the file's pages from the page cache (for cold-read measurements).
 void drop_cache(const DataFile& f);

@@ -205,7 +205,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     bool stop = false;
     int32_t err = SLLM_OK;
     std::string err_msg;
-    uint64_t bytes_read = 0;
+    uint64_t bytes_read = 0, bytes_bounced = 0;
 
     auto set_error = [&](int32_t st) {  // caller holds mu
         if (err == SLLM_OK) {
@@ -238,7 +238,8 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
                 s.pending = false;
             }
             const uint64_t off = k * C, len = std::min(C, read_end - off);
-            if (st == SLLM_OK) st = pread_full(h->file, s.host, len, off, h->data_path);
+            uint64_t bounced = 0;
+            if (st == SLLM_OK) st = read_chunk(h->file, s.host, len, off, h->data_path, &bounced);
             std::lock_guard<std::mutex> g(mu);
             if (st != SLLM_OK) {
                 free_q.push_back(si);
@@ -246,6 +247,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
                 return;
             }
             bytes_read += len;
+            bytes_bounced += bounced;
             ready_q.emplace_back(k, si);
             cv_ready.notify_one();
         }
@@ -295,6 +297,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     for (auto& t : threads) t.join();
     h->stats.read_wait_s = wait_s;
     h->stats.bytes_read = bytes_read;
+    h->stats.bytes_bounced = bytes_bounced;
     h->stats.n_launches = n;
     if (err != SLLM_OK) {
         for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);  // drain in-flight copies
@@ -471,6 +474,7 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
     h->stats.n_launches = 0;
     h->stats.from_cache = 0;
     h->stats.read_wait_s = 0;
+    h->stats.bytes_bounced = 0;
     h->stats.device_ms = -1;
     h->timed = false;
     const bool timing = (h->flags & SLLM_OPEN_TIMING) != 0;

@@ -241,7 +241,7 @@ extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_th
     const uint64_t read_end = f.direct ? ix.file_bytes : ix.total;
     int32_t st = parallel_chunks(n, io_threads ? io_threads : 4, -1, [&](uint64_t k) {
         const uint64_t off = k * C;
-        return pread_full(f, p->host[ids[k]], std::min(C, read_end - off), off, data_path);
+        return read_chunk(f, p->host[ids[k]], std::min(C, read_end - off), off, data_path, nullptr);
     });
     if (st != SLLM_OK) {
         give_back();

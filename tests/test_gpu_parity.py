@@ -313,3 +313,29 @@ def test_io_error_mid_load(torch_cuda, tmp_path):
         with open(path, "wb") as f:
             f.write(full)
         assert_same(run_load(torch, ck, len(want)), want, "after restoring the file")
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+def test_direct_io(torch_cuda, opt125m, engine):
+    """O_DIRECT reads (straight into pinned chunks, or through the bounce
+    buffer where the kernel refuses that) give the same bytes."""
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, index = expected(tensors, spec.alignment)
+    say("direct io", engine)
+    with binding.Checkpoint(d, engine=engine, direct_io=True, chunk_size=1 << 20, io_threads=4) as ck:
+        assert_same(run_load(torch, ck, len(want)), want, "direct streamed")
+        st = ck.stats()
+        if st["direct_io"]:
+            assert st["bytes_read"] == index.file_bytes  # direct reads run to the 4 KiB-padded end
+            assert st["bytes_bounced"] in (0, st["bytes_read"])
+    with binding.Pool(1 << 20, 300) as pool:
+        pool.cache(d, direct_io=True)
+        with binding.Checkpoint(d, pool=pool, engine=engine) as ck:
+            assert_same(run_load(torch, ck, len(want)), want, "direct cached")
+        pool.evict(d)
+
+
+def test_single_hip_runtime(torch_cuda):
+    """The library and torch share one HIP runtime (streams and pointers agree)."""
+    assert len(binding._hip_runtimes()) == 1
