@@ -112,15 +112,13 @@ uint32_t env_u32(const char* name, uint32_t dflt) {
 }  // namespace
 
 GatherShape gather_shape() {
-    static const GatherShape shape = [] {
-        GatherShape s;
-        s.blocks = env_u32("SLLM_K1_BLOCKS", 256);
-        s.unroll = env_u32("SLLM_K1_UNROLL", 1);
-        if (s.unroll != 1 && s.unroll != 2 && s.unroll != 4) s.unroll = 1;
-        s.nontemporal = env_u32("SLLM_K1_NT", 0) != 0;
-        return s;
-    }();
-    return shape;
+    // read at every launch (a few getenv calls) so one process can compare shapes
+    GatherShape s;
+    s.blocks = env_u32("SLLM_K1_BLOCKS", 512);
+    s.unroll = env_u32("SLLM_K1_UNROLL", 4);
+    if (s.unroll != 1 && s.unroll != 2 && s.unroll != 4) s.unroll = 4;
+    s.nontemporal = env_u32("SLLM_K1_NT", 0) != 0;
+    return s;
 }
 
 int32_t launch_gather(const GatherLaunch& g, hipStream_t stream) {

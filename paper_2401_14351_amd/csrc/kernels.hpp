@@ -24,8 +24,8 @@ struct GatherLaunch {
 };
 int32_t launch_gather(const GatherLaunch& g, hipStream_t stream);
 
-// Kernel launch shape knobs (read once from the environment:
-// SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT).
+// Kernel launch shape knobs, read from the environment at every launch:
+// SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT.
 struct GatherShape {
     uint32_t blocks;   // persistent grid size
     uint32_t unroll;   // 16-byte vectors per lane per tile: 1, 2 or 4

@@ -5,8 +5,8 @@
 //     wave, the 16 wave totals combined through LDS, a running carry across
 //     blocks of 1024 tensors.
 // K2  index-driven scatter (HBM source) and K1-scatter (mapped pinned host
-//     source): destination-driven.  Each workgroup owns a 16 KiB tile of the
-//     device image, finds the tensors whose slots meet the tile (binary
+//     source): destination-driven.  Each workgroup owns a 16 or 32 KiB tile
+//     of the device image, finds the tensors whose slots meet the tile (binary
 //     search of d), stages those index entries in LDS, and then every lane
 //     produces aligned 16-byte destination vectors: a straight 16-byte load
 //     when source and destination agree mod 16, two aligned loads and a byte
@@ -28,8 +28,6 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kThreads = 256;
-constexpr uint32_t kUnroll = 4;
-constexpr uint64_t kTile = (uint64_t)kThreads * 16 * kUnroll;  // destination bytes per tile
 constexpr uint32_t kLdsEntries = 256;                          // index entries staged per tile
 
 // ---------------------------------------------------------------------------
@@ -163,14 +161,27 @@ __device__ __forceinline__ uint64_t owner_global(const uint64_t* d, uint64_t lo,
     return lo;
 }
 
+template <bool NT>
+__device__ __forceinline__ void st16(uint8_t* p, u32x4 v) {
+    if constexpr (NT) {
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+    } else {
+        *reinterpret_cast<u32x4*>(p) = v;
+    }
+}
+
+// One tile: every lane first produces its U destination vectors (all source
+// loads in flight together), then stores them.
+template <uint32_t U, bool NT>
 __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
+    constexpr uint64_t kTileU = (uint64_t)kThreads * 16 * U;
     __shared__ uint64_t s_dev[kLdsEntries], s_off[kLdsEntries], s_size[kLdsEntries];
     __shared__ uint64_t s_lo, s_hi;
     const Src src{a};
     for (uint64_t t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
-        const uint64_t yt = (a.tile0 + t) * kTile;
+        const uint64_t yt = (a.tile0 + t) * kTileU;
         const uint64_t lo = yt > a.y0 ? yt : a.y0;
-        const uint64_t hi = yt + kTile < a.y1 ? yt + kTile : a.y1;
+        const uint64_t hi = yt + kTileU < a.y1 ? yt + kTileU : a.y1;
         if (threadIdx.x == 0) {
             const uint64_t i_lo = owner_global(a.dev, 0, a.n - 1, lo);
             s_lo = i_lo;
@@ -185,10 +196,14 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
             s_size[threadIdx.x] = a.size[i_lo + threadIdx.x];
         }
         __syncthreads();
+        u32x4 v[U];
+        uint32_t whole_mask = 0, in_mask = 0;
 #pragma unroll
-        for (uint32_t u = 0; u < kUnroll; ++u) {
+        for (uint32_t u = 0; u < U; ++u) {
+            v[u] = u32x4{0, 0, 0, 0};
             const uint64_t y = yt + ((uint64_t)u * kThreads + threadIdx.x) * 16;
             if (y + 16 <= lo || y >= hi) continue;
+            in_mask |= 1u << u;
             uint64_t dm, om, sm;
             if (cnt == 1) {
                 dm = s_dev[0]; om = s_off[0]; sm = s_size[0];
@@ -208,29 +223,33 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
             const uint32_t dn = sm > r ? (sm - r < 16 ? (uint32_t)(sm - r) : 16u) : 0u;  // data bytes in vector
             const uint64_t x = om + r;                   // source of the vector's first byte
             const bool whole = y >= lo && y + 16 <= hi;  // vector entirely ours to write
-            u32x4 v = u32x4{0, 0, 0, 0};
-            if (dn) {
-                const uint64_t xa = x & ~15ull;
-                const uint32_t sh = (uint32_t)(x & 15);
-                const uint64_t need = sh + dn > 16 ? 32 : 16;  // aligned source bytes spanned
-                if (whole && src.vectors_ok(xa, need)) {
-                    const u32x4 v0 = ld16(src.at(xa));
-                    v = sh == 0 ? v0 : funnel(v0, need == 32 ? ld16(src.at(xa + 16)) : v0, sh);
-                    if (dn < 16) v = keep_bytes(v, dn);
-                } else {
-                    uint32_t w[4] = {0, 0, 0, 0};
-                    for (uint32_t b = 0; b < dn; ++b) {
-                        if (y + b < lo || y + b >= hi) continue;
-                        w[b >> 2] |= (uint32_t)*src.at(x + b) << (8 * (b & 3));
-                    }
-                    v = u32x4{w[0], w[1], w[2], w[3]};
+            if (whole) whole_mask |= 1u << u;
+            if (!dn) continue;
+            const uint64_t xa = x & ~15ull;
+            const uint32_t sh = (uint32_t)(x & 15);
+            const uint64_t need = sh + dn > 16 ? 32 : 16;  // aligned source bytes spanned
+            if (whole && src.vectors_ok(xa, need)) {
+                const u32x4 v0 = ld16(src.at(xa));
+                u32x4 w = sh == 0 ? v0 : funnel(v0, need == 32 ? ld16(src.at(xa + 16)) : v0, sh);
+                v[u] = dn < 16 ? keep_bytes(w, dn) : w;
+            } else {
+                uint32_t w[4] = {0, 0, 0, 0};
+                for (uint32_t b = 0; b < dn; ++b) {
+                    if (y + b < lo || y + b >= hi) continue;
+                    w[b >> 2] |= (uint32_t)*src.at(x + b) << (8 * (b & 3));
                 }
+                v[u] = u32x4{w[0], w[1], w[2], w[3]};
             }
-            if (whole) {
-                *reinterpret_cast<u32x4*>(a.dst + y) = v;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < U; ++u) {
+            if (!(in_mask >> u & 1)) continue;
+            const uint64_t y = yt + ((uint64_t)u * kThreads + threadIdx.x) * 16;
+            if (whole_mask >> u & 1) {
+                st16<NT>(a.dst + y, v[u]);
             } else {
                 for (uint32_t b = 0; b < 16; ++b)
-                    if (y + b >= lo && y + b < hi) a.dst[y + b] = (uint8_t)byte_of(v, b);
+                    if (y + b >= lo && y + b < hi) a.dst[y + b] = (uint8_t)byte_of(v[u], b);
             }
         }
         __syncthreads();  // LDS entries are restaged for the next tile
@@ -252,6 +271,9 @@ uint64_t y_of(const DeviceLayout& l, uint64_t x) {
     return l.h_dev[i] + (x > l.h_off[i] ? x - l.h_off[i] : 0);
 }
 
+// Launch shape, read at every launch so that one process can compare shapes:
+// SLLM_K2_UNROLL (4 or 8 vectors per lane), SLLM_K2_NT (streaming stores),
+// SLLM_K2_BLOCKS / SLLM_K1_BLOCKS (grid for HBM / host sources).
 int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream_t stream) {
     a.off = l.d_off;
     a.size = l.d_size;
@@ -260,12 +282,21 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     a.total = l.total;
     if (a.y0 >= a.y1 || l.n == 0) return SLLM_OK;
     if (a.y1 > l.dev_total) return fail(SLLM_E_INVAL, "scatter: destination range past the image");
-    a.tile0 = a.y0 / kTile;
-    a.n_tiles = ceil_div(a.y1, kTile) - a.tile0;
+    const uint32_t unroll = env_blocks("SLLM_K2_UNROLL", 8) >= 8 ? 8 : 4;
+    const bool nt = env_blocks("SLLM_K2_NT", 0) == 1 && !src_is_host;
+    const uint64_t tile = (uint64_t)kThreads * 16 * unroll;
+    a.tile0 = a.y0 / tile;
+    a.n_tiles = ceil_div(a.y1, tile) - a.tile0;
     // host sources are PCIe-latency bound like K1; HBM sources want a full chip
-    const uint32_t want = src_is_host ? env_blocks("SLLM_K1_BLOCKS", 256) : env_blocks("SLLM_K2_BLOCKS", 2048);
-    const uint32_t grid = (uint32_t)std::min<uint64_t>(a.n_tiles, want);
-    k_scatter<<<dim3(grid), dim3(kThreads), 0, stream>>>(a);
+    const uint32_t want = src_is_host ? env_blocks("SLLM_K1_BLOCKS", 512) : env_blocks("SLLM_K2_BLOCKS", 1024);
+    const dim3 grid((uint32_t)std::min<uint64_t>(a.n_tiles, want)), block(kThreads);
+    if (unroll == 8) {
+        if (nt) k_scatter<8, true><<<grid, block, 0, stream>>>(a);
+        else k_scatter<8, false><<<grid, block, 0, stream>>>(a);
+    } else {
+        if (nt) k_scatter<4, true><<<grid, block, 0, stream>>>(a);
+        else k_scatter<4, false><<<grid, block, 0, stream>>>(a);
+    }
     SLLM_HIP(hipGetLastError());
     return SLLM_OK;
 }

@@ -183,13 +183,18 @@ def test_opt125m_file_layout(torch_cuda, opt125m, engine, cached):
 
 
 @pytest.mark.parametrize("engine", ["kernel", "sdma"])
-def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine):
+@pytest.mark.parametrize("shape", [{}, {"SLLM_K2_UNROLL": "4"}, {"SLLM_K2_NT": "1", "SLLM_K2_BLOCKS": "512"},
+                                   {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1", "SLLM_K1_BLOCKS": "96"}])
+def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine, shape, monkeypatch):
+    """Every launch shape of the scatter and gather kernels gives the same bytes."""
+    for k, v in shape.items():
+        monkeypatch.setenv(k, v)
     torch = torch_cuda
     spec, tensors, d = opt125m
     A2 = 4096
     want2, _ = expected(tensors, spec.alignment, A2)
     want1, _ = expected(tensors, spec.alignment)
-    say("opt-125m A2", engine)
+    say("opt-125m A2", engine, shape)
     with binding.Checkpoint(d, engine=engine, dev_alignment=A2) as ck:
         assert_same(run_load(torch, ck, len(want2)), want2, "A2 load")
         # the HBM-side repack (K2) of a file-layout image gives the same bytes
@@ -339,3 +344,21 @@ def test_direct_io(torch_cuda, opt125m, engine):
 def test_single_hip_runtime(torch_cuda):
     """The library and torch share one HIP runtime (streams and pointers agree)."""
     assert len(binding._hip_runtimes()) == 1
+
+
+@pytest.mark.parametrize("shape", [{"SLLM_K1_UNROLL": "2"}, {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1"},
+                                   {"SLLM_K1_BLOCKS": "1024"}, {"SLLM_K1_BLOCKS": "7", "SLLM_K1_UNROLL": "4"}])
+def test_gather_shapes(torch_cuda, opt125m, shape, monkeypatch):
+    """Every launch shape of the chunk gather gives the same bytes."""
+    for k, v in shape.items():
+        monkeypatch.setenv(k, v)
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, _ = expected(tensors, spec.alignment)
+    with binding.Pool(spec.chunk_size, 16) as pool:
+        pool.cache(d)
+        with binding.Checkpoint(d, pool=pool) as ck:
+            assert_same(run_load(torch, ck, len(want)), want, f"cached {shape}")
+        pool.evict(d)
+    with binding.Checkpoint(d, chunk_size=3 << 20) as ck:
+        assert_same(run_load(torch, ck, len(want)), want, f"streamed {shape}")
