@@ -36,6 +36,23 @@ PCIE_GEN5_X16_GBPS = 64.0   # MI355X host link: PCIe 5.0 x16, 32 GT/s x 16 lanes
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 
 
+def profiled_counters(summary: str, source: str):
+    """Counter figures recorded in profiles/<summary> ('counters: {json}' line),
+    or None when that file is missing or the kernel source has changed since
+    the counters were taken (its SHA-256 no longer matches)."""
+    path = os.path.join(ROOT, "profiles", summary)
+    if not os.path.exists(path):
+        return None
+    rec = None
+    for line in open(path):
+        if line.startswith("counters: "):
+            rec = json.loads(line[len("counters: "):])
+    if rec is None:
+        return None
+    src = open(os.path.join(ROOT, "paper_2401_14351_amd", "csrc", source), "rb").read()
+    return rec if hashlib.sha256(src).hexdigest() == rec.get("source_sha256") else None
+
+
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
@@ -160,9 +177,11 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
             if i:
                 ms.append(e0.elapsed_time(e1))
         k2 = (T + T2) / (statistics.mean(ms) * 1e-3) / 1e9
+        k2c = profiled_counters("k_scatter_repack_llama-2-7b.md", "layout.hip")
         out["repack_k2"] = {"dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
                             "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1),
-                            "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4)}
+                            "bound": "hbm", "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),
+                            "traffic": (k2c["fetch_bytes_per_launch"] + k2c["write_bytes_per_launch"]) if k2c else None}
         del dst
     log("repack:", out["repack_k2"])
     # streamed from the file with direct I/O through an 8-slot ring (cold: O_DIRECT bypasses the page cache)
@@ -276,7 +295,7 @@ def main():
     k_avg_s = statistics.mean(kernel_ms) * 1e-3
     achieved = T / k_avg_s / 1e9
     value = T * args.steps / elapsed / 1e9
-    profile_traffic = None
+    k1_counters = profiled_counters("k1_gather_llama-2-7b.md", "kernels.hip")
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -295,7 +314,10 @@ def main():
         "time_to_ready_s": round(statistics.median(ready), 5),
         "load_GBps": round(T / statistics.median(loads) / 1e9, 3),
         "roofline": {"bound": "pcie", "achieved": round(achieved, 3), "peak": PCIE_GEN5_X16_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / PCIE_GEN5_X16_GBPS, 4), "traffic": profile_traffic,
+                     "frac": round(achieved / PCIE_GEN5_X16_GBPS, 4),
+                     "traffic": k1_counters["fetch_bytes_per_launch"] if k1_counters else None,
+                     "traffic_write": k1_counters["write_bytes_per_launch"] if k1_counters else None,
+                     "algorithmic_bytes": T,
                      "kernel": "k1_gather", "kernel_ms": round(statistics.mean(kernel_ms), 3),
                      "peak_measured": None if h2d_peak is None else round(h2d_peak, 3),
                      "frac_measured": None if h2d_peak is None else round(achieved / h2d_peak, 4),
