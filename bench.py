@@ -34,6 +34,12 @@ from paper_2401_14351_amd import binding, synth  # noqa: E402
 METRIC = "checkpoint load GB/s host DRAM→HBM + time-to-ready (s), 7B-shaped bf16"
 PCIE_GEN5_X16_GBPS = 64.0   # MI355X host link: PCIe 5.0 x16, 32 GT/s x 16 lanes per direction
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
+DATA = {"llama": "synthetic (seeded N(0,0.02) bf16 weights, RMSNorm weights 1.0)",
+        "opt-125m": "synthetic (seeded N(0,0.02) fp16 weights)",
+        "stress": "synthetic (seeded uniform random bytes, f32/f16/bf16/i8 tensors)"}
+REGIME = {"dram": "warm host DRAM (pinned pool)",
+          "ring": "file through pinned ring slots (buffered reads)",
+          "direct": "file through pinned ring slots (O_DIRECT reads)"}
 
 
 def profiled_counters(summary: str, source: str):
@@ -205,6 +211,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama-2-7b", choices=list(synth.WORKLOADS) + ["stress-8g"])
     ap.add_argument("--engine", default="kernel", choices=["kernel", "sdma"])
+    ap.add_argument("--regime", default="dram", choices=["dram", "ring", "direct"],
+                    help="dram: partition cached in the pinned pool (graded); ring: streamed from the file "
+                         "through pinned slots (buffered reads); direct: the same with O_DIRECT reads")
+    ap.add_argument("--chunk-size", type=int, default=0, help="chunk size in bytes (default: the workload's)")
+    ap.add_argument("--io-threads", type=int, default=8)
+    ap.add_argument("--ring-slots", type=int, default=32)
     ap.add_argument("--dir", default=None, help="where the converted checkpoint lives")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle reading")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -235,18 +247,26 @@ def main():
     h2d_peak, hbm_peak = (None, None) if args.no_peaks else measure_peaks(torch)
     log(f"measured peaks: pinned->HBM copy {h2d_peak} GB/s, HBM copy {hbm_peak} GB/s")
 
-    C = spec.chunk_size
+    C = args.chunk_size or spec.chunk_size
     with binding.Checkpoint(d) as probe:
         T = probe.total_bytes
     n_chunks = -(-T // C)
+    cached = args.regime == "dram"
     t0 = time.time()
-    pool = binding.Pool(C, n_chunks)
-    log(f"pinned pool: {n_chunks} x {C >> 20} MiB in {time.time() - t0:.1f} s")
-    t0 = time.time()
-    pool.cache(d, io_threads=8)
-    fill_s = time.time() - t0
-    log(f"DRAM tier filled in {fill_s:.1f} s")
+    pool = binding.Pool(C, n_chunks if cached else args.ring_slots)
+    log(f"pinned pool: {n_chunks if cached else args.ring_slots} x {C / 2**20:g} MiB in {time.time() - t0:.1f} s")
+    fill_s = None
+    if cached:
+        t0 = time.time()
+        pool.cache(d, io_threads=args.io_threads)
+        fill_s = time.time() - t0
+        log(f"DRAM tier filled in {fill_s:.1f} s")
+    open_kw = dict(pool=pool, engine=args.engine)
+    if not cached:
+        open_kw.update(chunk_size=C, io_threads=args.io_threads, ring_slots=args.ring_slots,
+                       direct_io=args.regime == "direct")
     buf = torch.empty(T, dtype=torch.uint8, device="cuda:0")
+    last_stats = {}
 
     ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -254,7 +274,7 @@ def main():
 
     def step(i=None):
         t_open = time.perf_counter()
-        ck = binding.Checkpoint(d, pool=pool, engine=args.engine)
+        ck = binding.Checkpoint(d, **open_kw)
         t_load = time.perf_counter()
         if i is not None:
             ev0[i].record(stream)
@@ -264,6 +284,7 @@ def main():
         views = binding.views(buf, ck.tensors())
         stream.synchronize()
         t_end = time.perf_counter()
+        last_stats.update(ck.stats())
         ck.close()
         return t_end - t_open, t_end - t_load, views
 
@@ -287,15 +308,24 @@ def main():
             if got.tobytes() != want.tobytes():
                 raise SystemExit(f"bench: tensor {names[i]} differs from the generator's bytes")
     del views
-    extras = {} if args.no_extras else measure_extras(torch, spec, d, pool, buf, stream, args.engine)
-    extras["dram_tier_fill"] = {"GBps": round(T / fill_s / 1e9, 3), "s": round(fill_s, 3), "io_threads": 8,
-                                "source": "converted file, page cache warm"}
+    extras = {} if (args.no_extras or not cached) else measure_extras(torch, spec, d, pool, buf, stream, args.engine)
+    if fill_s is not None:
+        extras["dram_tier_fill"] = {"GBps": round(T / fill_s / 1e9, 3), "s": round(fill_s, 3),
+                                    "io_threads": args.io_threads, "source": "converted file, page cache warm"}
+    if not cached:
+        extras["ring"] = {"io_threads": args.io_threads, "ring_slots": args.ring_slots,
+                          "direct_io": int(last_stats.get("direct_io", 0)),
+                          "bytes_read": int(last_stats.get("bytes_read", 0)),
+                          "bytes_bounced": int(last_stats.get("bytes_bounced", 0)),
+                          "read_wait_s": round(last_stats.get("read_wait_s", 0.0), 4),
+                          "device": block_device(d)}
 
     kernel_ms = [a.elapsed_time(b) for a, b in zip(ev0, ev1)]
     k_avg_s = statistics.mean(kernel_ms) * 1e-3
     achieved = T / k_avg_s / 1e9
     value = T * args.steps / elapsed / 1e9
-    k1_counters = profiled_counters("k1_gather_llama-2-7b.md", "kernels.hip")
+    k1_counters = (profiled_counters("k1_gather_llama-2-7b.md", "kernels.hip")
+                   if cached and args.engine == "kernel" and spec.name == "llama-2-7b" and C == 16 << 20 else None)
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -308,9 +338,9 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u8",
-        "data": "synthetic (seeded N(0,0.02) bf16 weights, RMSNorm weights 1.0)",
+        "data": DATA.get(spec.name.split("-cap")[0], DATA["llama"]),
         "config": {"workload": spec.name, "bytes": T, "tensors": len(spec.tensors), "chunk_size": C,
-                   "alignment": spec.alignment, "engine": args.engine, "regime": "warm host DRAM (pinned pool)"},
+                   "alignment": spec.alignment, "engine": args.engine, "regime": REGIME[args.regime]},
         "time_to_ready_s": round(statistics.median(ready), 5),
         "load_GBps": round(T / statistics.median(loads) / 1e9, 3),
         "roofline": {"bound": "pcie", "achieved": round(achieved, 3), "peak": PCIE_GEN5_X16_GBPS, "unit": "GB/s",
@@ -318,7 +348,9 @@ def main():
                      "traffic": k1_counters["fetch_bytes_per_launch"] if k1_counters else None,
                      "traffic_write": k1_counters["write_bytes_per_launch"] if k1_counters else None,
                      "algorithmic_bytes": T,
-                     "kernel": "k1_gather", "kernel_ms": round(statistics.mean(kernel_ms), 3),
+                     "kernel": ("k1_gather" if cached and args.engine == "kernel" else
+                                "whole load on the caller's stream (events around sllm_load)"),
+                     "kernel_ms": round(statistics.mean(kernel_ms), 3),
                      "peak_measured": None if h2d_peak is None else round(h2d_peak, 3),
                      "frac_measured": None if h2d_peak is None else round(achieved / h2d_peak, 4),
                      "hbm_copy_measured": None if hbm_peak is None else round(hbm_peak, 1)},
@@ -326,7 +358,8 @@ def main():
         "extras": extras,
     }
     print(json.dumps(out), flush=True)
-    pool.evict(d)
+    if cached:
+        pool.evict(d)
     pool.close()
     if args.calib_copy:
         del buf

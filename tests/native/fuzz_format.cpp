@@ -1,0 +1,117 @@
+// CPU-only driver for the host-side format code, built with AddressSanitizer
+// and UndefinedBehaviorSanitizer by tests/test_sanitize.py.
+//
+//  1. Random checkpoints go through the streaming writer; their index must
+//     decode, describe the aligned packed layout, and the data file must hold
+//     every tensor's bytes with zero padding.
+//  2. A valid index is mutated (byte flips, truncation, growth), with its CRC
+//     recomputed half of the time so that field validation is reached.  The
+//     decoder must never fault, and any index it accepts must re-encode to
+//     exactly the same bytes.
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <fstream>
+#include <random>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "format.hpp"
+#include "sllm.h"
+
+using namespace sllm;
+
+static std::string slurp(const std::string& path) {
+    std::ifstream f(path, std::ios::binary);
+    std::stringstream ss;
+    ss << f.rdbuf();
+    return ss.str();
+}
+
+#define CHECK(c)                                                             \
+    do {                                                                     \
+        if (!(c)) {                                                          \
+            std::fprintf(stderr, "check failed: %s (line %d)\n", #c, __LINE__); \
+            return 1;                                                        \
+        }                                                                    \
+    } while (0)
+
+int main(int argc, char** argv) {
+    if (argc < 3) return 2;
+    const std::string dir = argv[1];
+    const long iters = std::atol(argv[2]);
+    std::mt19937_64 rng(20240125);
+    std::string valid;
+
+    for (int round = 0; round < 60; ++round) {
+        sllm_convert_opts o{1ull << (rng() % 13), 1 + rng() % 5000, 0, 0};
+        sllm_writer* w = nullptr;
+        CHECK(sllm_writer_open(dir.c_str(), &o, &w) == SLLM_OK);
+        const int n = (int)(rng() % 24);
+        std::vector<std::vector<uint8_t>> data(n);
+        std::vector<uint64_t> sizes(n);
+        for (int i = 0; i < n; ++i) {
+            const uint32_t dtype = (uint32_t)(rng() % 4);
+            const uint32_t ndim = (uint32_t)(rng() % 4);
+            int64_t shape[4] = {1, 1, 1, 1};
+            uint64_t numel = 1;
+            for (uint32_t d = 0; d < ndim; ++d) {
+                shape[d] = (int64_t)(rng() % 9);
+                numel *= (uint64_t)shape[d];
+            }
+            sizes[i] = numel * itemsize(dtype);
+            data[i].resize(sizes[i]);
+            for (auto& b : data[i]) b = (uint8_t)(rng() & 0xFF);
+            const std::string name = "t" + std::to_string(round) + "." + std::to_string(i);
+            sllm_src_tensor t{name.c_str(), dtype, ndim, shape, data[i].data(), sizes[i]};
+            CHECK(sllm_writer_add(w, &t) == SLLM_OK);
+        }
+        CHECK(sllm_writer_close(w) == SLLM_OK);
+        const std::string blob = slurp(dir + "/sllm.index");
+        const std::string part = slurp(dir + "/sllm.part0");
+        IndexData ix;
+        CHECK(decode_index(blob.data(), blob.size(), &ix) == SLLM_OK);
+        CHECK(encode_index(ix) == blob);
+        std::vector<uint64_t> off(n);
+        uint64_t T = 0;
+        CHECK(plan_layout(sizes.data(), (size_t)n, o.alignment, off.data(), &T) == SLLM_OK);
+        CHECK(ix.total == T && part.size() == ix.file_bytes && ix.file_bytes % 4096 == 0 && ix.file_bytes - T < 4096);
+        std::vector<uint8_t> used(part.size(), 0);
+        for (int i = 0; i < n; ++i) {
+            CHECK(ix.tensors[i].offset == off[i] && ix.tensors[i].nbytes == sizes[i]);
+            if (!sizes[i]) continue;
+            CHECK(std::memcmp(part.data() + off[i], data[i].data(), sizes[i]) == 0);
+            std::memset(used.data() + off[i], 1, sizes[i]);
+        }
+        for (size_t x = 0; x < part.size(); ++x) CHECK(used[x] || part[x] == 0);
+        if (n > 3) valid = blob;
+    }
+    CHECK(!valid.empty());
+
+    long accepted = 0;
+    for (long it = 0; it < iters; ++it) {
+        std::string m = valid;
+        const int kind = (int)(rng() % 4);
+        if (kind == 0) {
+            m.resize(rng() % (m.size() + 1));
+        } else if (kind == 1) {
+            const size_t extra = 1 + rng() % 64;
+            for (size_t k = 0; k < extra; ++k) m.insert(m.begin() + (long)(rng() % (m.size() + 1)), (char)(rng() & 0xFF));
+        } else {
+            const int flips = 1 + (int)(rng() % 4);
+            for (int k = 0; k < flips; ++k) m[rng() % m.size()] ^= (char)(1u << (rng() % 8));
+        }
+        if ((rng() & 1) && m.size() >= 4) {  // recompute the CRC so the fields themselves are checked
+            const uint32_t c = crc32(m.data(), m.size() - 4);
+            std::memcpy(&m[m.size() - 4], &c, 4);
+        }
+        IndexData ix;
+        if (decode_index(m.data(), m.size(), &ix) == SLLM_OK) {
+            ++accepted;
+            CHECK(encode_index(ix) == m);
+        }
+    }
+    std::printf("ok rounds=60 mutants=%ld accepted=%ld\n", iters, accepted);
+    return 0;
+}
