@@ -160,6 +160,10 @@ int32_t sllm_pool_evict(sllm_pool* pool, const char* dir);
 #define SLLM_OPEN_DIRECT_IO 1u  /* O_DIRECT file reads (buffered if the file
                                    system refuses them; see stats.direct_io) */
 #define SLLM_OPEN_TIMING    2u  /* time device work with HIP events (stats)   */
+#define SLLM_OPEN_INDEX_ONLY 4u /* read and validate the index only: no data
+                                   file, pool or device work; for processes
+                                   that view a buffer another process loaded
+                                   (sllm_load then returns SLLM_E_INVAL)      */
 
 typedef struct sllm_open_opts {
     uint64_t   chunk_size;     /* C for reads from the file; 0 = pool's chunk
@@ -250,6 +254,83 @@ typedef struct sllm_stats {
                                    into the pinned chunks                      */
 } sllm_stats;
 int32_t sllm_get_stats(const sllm_ckpt* h, sllm_stats* out);
+
+/* =========================================================================
+ * Handoff to another process (Sec. 4.1: the model manager loads, the
+ * inference process receives the GPU base address as an IPC handle, computes
+ * base + offset from the index and synchronizes with the manager)
+ * ========================================================================= */
+
+typedef struct sllm_ipc_desc {
+    uint8_t  mem_handle[64];    /* IPC handle of the allocation holding the buffer */
+    uint8_t  event_handle[64];  /* IPC handle of an event recorded after the load  */
+    uint64_t offset;            /* start of the buffer inside that allocation      */
+    uint64_t bytes;             /* length of the buffer                            */
+    int32_t  device;
+    uint32_t reserved;
+} sllm_ipc_desc;
+
+/* Largest allocation this library shares across processes: opening handles
+ * of larger allocations does not complete on the MI355X systems it was
+ * tested on, so export refuses them. */
+#define SLLM_IPC_MAX_ALLOCATION ((2ull << 30) - 1)
+
+typedef struct sllm_export sllm_export;
+typedef struct sllm_import sllm_import;
+
+/* Share [dev_ptr, dev_ptr + bytes) (inside one device allocation of at most
+ * SLLM_IPC_MAX_ALLOCATION bytes) with other processes: fills *desc (plain
+ * bytes, safe to send through a pipe or file) and records the handoff event
+ * on `stream`, after the work already queued there (typically sllm_load).
+ * Keep the export alive while importers use the buffer.
+ * Errors: INVAL (not device memory, allocation too large, range outside it), HIP. */
+int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32_t device, void* stream,
+                           sllm_ipc_desc* desc, sllm_export** out);
+int32_t sllm_export_destroy(sllm_export* ex);
+
+/* Map an exported buffer into this process: *dev_ptr is its start here, and
+ * `stream` waits (on the device) for the exporter's handoff event, so work
+ * queued on it afterwards sees the loaded bytes.  Errors: INVAL, HIP. */
+int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, void** dev_ptr, sllm_import** out);
+/* Unmap; work that reads the buffer must have finished. */
+int32_t sllm_import_close(sllm_import* im);
+
+/* =========================================================================
+ * Loading-time estimate (Sec. 6, estimating model loading time): a load of
+ * n bytes queued behind other loads on this server finishes after q + n / b,
+ * where q sums the estimates of the loads already queued (loads run one at a
+ * time per server) and b is the bandwidth of the slowest tier the load
+ * crosses (the tiers are pipelined).  Measured load times refine b.
+ * Host-only; no device work.
+ * ========================================================================= */
+
+#define SLLM_TIER_DRAM    1u  /* pinned host DRAM -> HBM        */
+#define SLLM_TIER_STORAGE 2u  /* local file -> pinned host DRAM */
+
+typedef struct sllm_estimator sllm_estimator;
+
+/* Initial bandwidths in bytes per second (> 0) and the weight in (0, 1] of a
+ * new measurement in the running estimate (1 = keep only the latest). */
+int32_t sllm_estimator_create(double dram_bytes_per_s, double storage_bytes_per_s, double weight,
+                              sllm_estimator** out);
+void    sllm_estimator_destroy(sllm_estimator* e);
+
+/* q + n / b for a load of `bytes` crossing `tiers` (SLLM_TIER_* bits),
+ * queued behind every load enqueued and not yet completed. */
+int32_t sllm_estimator_query(const sllm_estimator* e, uint64_t bytes, uint32_t tiers, double* eta_s);
+
+/* Queue such a load: *eta_s is its estimate (as for query) and *task its id;
+ * its own n / b joins q for the loads queued after it. */
+int32_t sllm_estimator_enqueue(sllm_estimator* e, uint64_t bytes, uint32_t tiers, uint64_t* task,
+                               double* eta_s);
+
+/* The task's load took `seconds`: bytes / seconds updates the bandwidth of
+ * its slowest tier and the task leaves the queue.  NOTFOUND for an unknown
+ * task, INVAL for seconds <= 0. */
+int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, double seconds);
+
+/* Current bandwidth estimate of one tier (bytes per second). */
+int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bytes_per_s);
 
 /* Close the handle; waits for its in-flight device work first. */
 int32_t sllm_close(sllm_ckpt* h);

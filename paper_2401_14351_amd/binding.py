@@ -27,6 +27,7 @@ ITEMSIZE = {0: 4, 1: 2, 2: 2, 3: 1}
 ENGINE = {"kernel": 0, "sdma": 1}
 OPEN_DIRECT_IO = 1
 OPEN_TIMING = 2
+OPEN_INDEX_ONLY = 4
 CONVERT_FSYNC = 1
 MAX_NDIM = 8
 
@@ -64,6 +65,11 @@ class Stats(C.Structure):
                 ("bytes_bounced", C.c_uint64)]
 
 
+class IpcDesc(C.Structure):
+    _fields_ = [("mem_handle", C.c_uint8 * 64), ("event_handle", C.c_uint8 * 64), ("offset", C.c_uint64),
+                ("bytes", C.c_uint64), ("device", C.c_int32), ("reserved", C.c_uint32)]
+
+
 # name -> (restype, argtypes); every symbol the header declares
 SIGNATURES = {
     "sllm_convert": (C.c_int32, [C.POINTER(SrcTensor), C.c_uint64, C.c_char_p, C.POINTER(ConvertOpts)]),
@@ -84,6 +90,18 @@ SIGNATURES = {
     "sllm_tensor_find": (C.c_int32, [C.c_void_p, C.c_char_p, C.POINTER(TensorInfo)]),
     "sllm_get_stats": (C.c_int32, [C.c_void_p, C.POINTER(Stats)]),
     "sllm_close": (C.c_int32, [C.c_void_p]),
+    "sllm_export_create": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_int32, C.c_void_p, C.POINTER(IpcDesc),
+                                       C.POINTER(C.c_void_p)]),
+    "sllm_export_destroy": (C.c_int32, [C.c_void_p]),
+    "sllm_import_open": (C.c_int32, [C.POINTER(IpcDesc), C.c_void_p, C.POINTER(C.c_void_p), C.POINTER(C.c_void_p)]),
+    "sllm_import_close": (C.c_int32, [C.c_void_p]),
+    "sllm_estimator_create": (C.c_int32, [C.c_double, C.c_double, C.c_double, C.POINTER(C.c_void_p)]),
+    "sllm_estimator_destroy": (None, [C.c_void_p]),
+    "sllm_estimator_query": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_uint32, C.POINTER(C.c_double)]),
+    "sllm_estimator_enqueue": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_uint32, C.POINTER(C.c_uint64),
+                                           C.POINTER(C.c_double)]),
+    "sllm_estimator_complete": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_double]),
+    "sllm_estimator_bandwidth": (C.c_int32, [C.c_void_p, C.c_uint32, C.POINTER(C.c_double)]),
     "sllm_last_error": (C.c_char_p, []),
     "sllm_strerror": (C.c_char_p, [C.c_int32]),
 }
@@ -264,8 +282,9 @@ class Checkpoint:
 
     def __init__(self, ckpt_dir: str, device: int = 0, pool: Optional[Pool] = None, chunk_size: int = 0,
                  dev_alignment: int = 0, io_threads: int = 4, n_streams: int = 2, ring_slots: int = 0,
-                 engine: str = "kernel", direct_io: bool = False, timing: bool = False):
-        flags = (OPEN_DIRECT_IO if direct_io else 0) | (OPEN_TIMING if timing else 0)
+                 engine: str = "kernel", direct_io: bool = False, timing: bool = False, index_only: bool = False):
+        flags = (OPEN_DIRECT_IO if direct_io else 0) | (OPEN_TIMING if timing else 0) | \
+            (OPEN_INDEX_ONLY if index_only else 0)
         opts = OpenOpts(chunk_size, dev_alignment, pool.handle if pool else None, io_threads, n_streams,
                         ring_slots, ENGINE[engine], flags, device)
         self._h = C.c_void_p()
@@ -358,3 +377,99 @@ def load(ckpt_dir: str, device: int = 0, stream=None, pool: Optional[Pool] = Non
         out = views(buf, ck.tensors())
         s.synchronize()
     return buf, out
+
+
+def device_tensor(ptr: int, nbytes: int, device: int = 0):
+    """A uint8 torch tensor over device memory this process did not allocate
+    (an imported buffer), through the CUDA array interface."""
+    import torch
+
+    class _Mem:
+        __cuda_array_interface__ = {"shape": (nbytes,), "typestr": "|u1", "data": (ptr, False), "version": 3}
+
+    return torch.as_tensor(_Mem(), device=f"cuda:{device}")
+
+
+class Export:
+    """Share a loaded uint8 device buffer with another process (``sllm_export_*``).
+
+    The handoff event is recorded on ``stream`` after the work queued there,
+    so export right after ``Checkpoint.load_into(buf, stream)``."""
+
+    def __init__(self, buf, stream=None, device: int = 0):
+        self.desc = IpcDesc()
+        self._h = C.c_void_p()
+        check(lib().sllm_export_create(buf.data_ptr(), buf.numel(), device, _stream_ptr(stream), C.byref(self.desc),
+                                       C.byref(self._h)))
+        self._buf = buf  # the shared memory must outlive the export
+
+    @property
+    def desc_bytes(self) -> bytes:
+        return bytes(self.desc)
+
+    def close(self) -> None:
+        if self._h:
+            check(lib().sllm_export_destroy(self._h))
+            self._h = C.c_void_p()
+            self._buf = None
+
+
+class Import:
+    """Map a buffer exported by another process; ``stream`` waits for its load."""
+
+    def __init__(self, desc: bytes, stream=None):
+        if len(desc) != C.sizeof(IpcDesc):
+            raise ValueError("not an sllm_ipc_desc")
+        self.desc = IpcDesc.from_buffer_copy(desc)
+        ptr, self._h = C.c_void_p(), C.c_void_p()
+        check(lib().sllm_import_open(C.byref(self.desc), _stream_ptr(stream), C.byref(ptr), C.byref(self._h)))
+        self.ptr = ptr.value
+
+    def tensor(self):
+        return device_tensor(self.ptr, self.desc.bytes, self.desc.device)
+
+    def close(self) -> None:
+        if self._h:
+            check(lib().sllm_import_close(self._h))
+            self._h = C.c_void_p()
+
+
+TIER_DRAM = 1
+TIER_STORAGE = 2
+
+
+class Estimator:
+    """Loading-time estimate q + n / b (``sllm_estimator_*``)."""
+
+    def __init__(self, dram_bytes_per_s: float, storage_bytes_per_s: float, weight: float = 0.5):
+        self._h = C.c_void_p()
+        check(lib().sllm_estimator_create(dram_bytes_per_s, storage_bytes_per_s, weight, C.byref(self._h)))
+
+    def query(self, nbytes: int, tiers: int) -> float:
+        out = C.c_double()
+        check(lib().sllm_estimator_query(self._h, int(nbytes), tiers, C.byref(out)))
+        return out.value
+
+    def enqueue(self, nbytes: int, tiers: int) -> Tuple[int, float]:
+        task, eta = C.c_uint64(), C.c_double()
+        check(lib().sllm_estimator_enqueue(self._h, int(nbytes), tiers, C.byref(task), C.byref(eta)))
+        return task.value, eta.value
+
+    def complete(self, task: int, seconds: float) -> None:
+        check(lib().sllm_estimator_complete(self._h, task, seconds))
+
+    def bandwidth(self, tier: int) -> float:
+        out = C.c_double()
+        check(lib().sllm_estimator_bandwidth(self._h, tier, C.byref(out)))
+        return out.value
+
+    def close(self) -> None:
+        if self._h:
+            lib().sllm_estimator_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -65,7 +65,9 @@ struct sllm_ckpt {
 namespace {
 
 void release(sllm_ckpt* h) {
-    {
+    const bool used_hip = !h->streams.empty() || !h->slots.empty() || h->fork_ev || h->t0_ev || h->t1_ev ||
+                          h->layout.d_off || h->layout.staging;
+    if (used_hip) {
         DeviceGuard guard(h->device);
         for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
         for (Slot& s : h->slots)
@@ -316,7 +318,8 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
     sllm_open_opts o{};
     if (opts) o = *opts;
     if (o.engine != SLLM_ENGINE_KERNEL && o.engine != SLLM_ENGINE_SDMA) return fail(SLLM_E_INVAL, "unknown engine %u", o.engine);
-    if (o.flags & ~(SLLM_OPEN_DIRECT_IO | SLLM_OPEN_TIMING)) return fail(SLLM_E_INVAL, "unknown flags 0x%x", o.flags);
+    if (o.flags & ~(SLLM_OPEN_DIRECT_IO | SLLM_OPEN_TIMING | SLLM_OPEN_INDEX_ONLY))
+        return fail(SLLM_E_INVAL, "unknown flags 0x%x", o.flags);
     if (o.dev_alignment && (!is_pow2(o.dev_alignment) || o.dev_alignment < 16))
         return fail(SLLM_E_INVAL, "device alignment %llu is not a power of two >= 16", (unsigned long long)o.dev_alignment);
     if (o.pool && o.pool->device != o.device)
@@ -342,9 +345,11 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
     std::string blob;
     int32_t st = read_small_file(std::string(dir) + "/" + kIndexName, &blob);
     if (st == SLLM_OK) st = decode_index(blob.data(), blob.size(), &h->ix);
-    if (st == SLLM_OK) st = open_data(h->data_path, (o.flags & SLLM_OPEN_DIRECT_IO) != 0, &h->file);
     if (st != SLLM_OK) return bail(st);
-    if (h->file.size != h->ix.file_bytes) {
+    const bool index_only = (o.flags & SLLM_OPEN_INDEX_ONLY) != 0;
+    if (!index_only) st = open_data(h->data_path, (o.flags & SLLM_OPEN_DIRECT_IO) != 0, &h->file);
+    if (st != SLLM_OK) return bail(st);
+    if (!index_only && h->file.size != h->ix.file_bytes) {
         fail(SLLM_E_FORMAT, "%s is %llu bytes, the index says %llu", h->data_path.c_str(),
              (unsigned long long)h->file.size, (unsigned long long)h->ix.file_bytes);
         return bail(SLLM_E_FORMAT);
@@ -363,6 +368,13 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
     } else {
         for (size_t i = 0; i < nt; ++i) h->dev_off[i] = h->ix.tensors[i].offset;
         h->dev_total = h->ix.total;
+    }
+
+    if (index_only) {
+        h->stats.device_ms = -1;
+        h->stats.open_s = now_s() - t0;
+        *out = h;
+        return SLLM_OK;
     }
 
     // the chunk pool: a shared one (maybe caching this partition) or a private ring
@@ -459,6 +471,7 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
         std::atomic<bool>* b;
         ~Unbusy() { b->store(false); }
     } unbusy{&h->busy};
+    if (h->flags & SLLM_OPEN_INDEX_ONLY) return fail(SLLM_E_INVAL, "the handle was opened for its index only");
     if (!dev_dst && h->dev_total) return fail(SLLM_E_INVAL, "destination is NULL");
     if (reinterpret_cast<uintptr_t>(dev_dst) % 16) return fail(SLLM_E_INVAL, "destination is not 16-byte aligned");
     if (dst_bytes < h->dev_total)
@@ -499,6 +512,7 @@ extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t
     clear_error();
     if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
     if (!h->dev_align) return fail(SLLM_E_INVAL, "the handle was opened without a device alignment");
+    if (h->flags & SLLM_OPEN_INDEX_ONLY) return fail(SLLM_E_INVAL, "the handle was opened for its index only");
     if (src_bytes < h->ix.total || dst_bytes < h->dev_total)
         return fail(SLLM_E_RANGE, "repack needs %llu source and %llu destination bytes", (unsigned long long)h->ix.total,
                     (unsigned long long)h->dev_total);

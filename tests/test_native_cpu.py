@@ -48,7 +48,8 @@ def test_struct_layouts_match_header(tmp_path):
     probe = tmp_path / "probe.c"
     structs = {"sllm_src_tensor": binding.SrcTensor, "sllm_convert_opts": binding.ConvertOpts,
                "sllm_pool_info": binding.PoolInfo, "sllm_open_opts": binding.OpenOpts,
-               "sllm_tensor_info": binding.TensorInfo, "sllm_stats": binding.Stats}
+               "sllm_tensor_info": binding.TensorInfo, "sllm_stats": binding.Stats,
+               "sllm_ipc_desc": binding.IpcDesc}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "sllm.h"', "int main(void) {"]
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
@@ -263,3 +264,24 @@ def test_open_rejects_bad_options(L, ckpt):
         for k, v in kw.items():
             setattr(o, k, v)
         assert L.sllm_open(str(ckpt).encode(), C.byref(o), C.byref(h)) == -1, kw
+
+
+@pytest.mark.parametrize("A,A2", [(1, 0), (16, 0), (4096, 0), (1, 16), (16, 256), (4096, 256), (256, 4096)])
+def test_index_only_open_matches_oracle_layout(L, tmp_path, A, A2):
+    """An index-only handle needs no GPU; its offsets are the oracle's (file
+    layout, or the A2 device layout planned on the host)."""
+    spec = synth.tiny(9, alignment=A)
+    tensors = _tensors(spec)
+    oracle.convert(tensors, str(tmp_path), A, 64)
+    index = oracle.read_index(str(tmp_path))
+    want, total = (oracle.device_layout(index, A2) if A2 else
+                   ([e.offset for e in index.entries], index.total_bytes))
+    with binding.Checkpoint(str(tmp_path), index_only=True, dev_alignment=A2) as ck:
+        got = ck.tensors()
+        assert [t.offset for t in got] == want and ck.total_bytes == total
+        assert [(t.name, t.dtype, t.shape, t.nbytes) for t in got] == \
+            [(e.name, e.dtype, e.shape, e.nbytes) for e in index.entries]
+        assert ck.find(index.entries[-1].name).offset == want[-1]
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load(0, 1 << 30)
+        assert ei.value.code == -1
