@@ -36,7 +36,8 @@ PCIE_GEN5_X16_GBPS = 64.0   # MI355X host link: PCIe 5.0 x16, 32 GT/s x 16 lanes
 HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 DATA = {"llama": "synthetic (seeded N(0,0.02) bf16 weights, RMSNorm weights 1.0)",
         "opt-125m": "synthetic (seeded N(0,0.02) fp16 weights)",
-        "stress": "synthetic (seeded uniform random bytes, f32/f16/bf16/i8 tensors)"}
+        "stress": "synthetic (seeded uniform random bytes, f32/f16/bf16/i8 tensors)",
+        "lora": "synthetic (seeded N(0,0.02) bf16 LoRA A/B matrices)"}
 REGIME = {"dram": "warm host DRAM (pinned pool)",
           "ring": "file through pinned ring slots (buffered reads)",
           "direct": "file through pinned ring slots (O_DIRECT reads)"}
@@ -138,6 +139,65 @@ def cpu_baseline(d: str, budget_s: float):
                       f"chunks ({nbytes / 1e9:.2f} GB) in {dt:.1f} s on one core"}
 
 
+def storage_peak(path: str, block: int = 4 << 20, depth: int = 32, budget_s: float = 4.0):
+    """Direct sequential reads of `block` bytes with `depth` requests in flight
+    (the storage peak the paper measures with FIO: 4 MiB, direct, depth 32),
+    over the checkpoint's own data file.  None if the file system refuses
+    O_DIRECT."""
+    import itertools
+    import mmap
+    import threading
+
+    try:
+        fd = os.open(path, os.O_RDONLY | os.O_DIRECT)
+    except OSError:
+        return None
+    try:
+        nblocks = os.fstat(fd).st_size // block
+        if nblocks == 0:
+            return None
+        counter = itertools.count()
+        total = [0] * depth
+        deadline = time.perf_counter() + budget_s
+
+        def worker(i):
+            buf = mmap.mmap(-1, block)
+            while time.perf_counter() < deadline:
+                k = next(counter) % nblocks
+                total[i] += os.preadv(fd, [buf], k * block)
+
+        t0 = time.perf_counter()
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(depth)]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        dt = time.perf_counter() - t0
+        return {"GBps": round(sum(total) / dt / 1e9, 3), "block": block, "depth": depth,
+                "bytes": sum(total), "device": block_device(path)}
+    finally:
+        os.close(fd)
+
+
+def estimator_replay(ready, T, tiers, dram_bps, storage_bps):
+    """Feed the measured steps, in order, to the loading-time estimator
+    (q + n / b, refined from each completed load) and report how far each
+    prediction made before a step was from that step's time-to-ready."""
+    est = binding.Estimator(dram_bps, storage_bps, weight=0.5)
+    err = []
+    for r in ready:
+        task, eta = est.enqueue(T, tiers)
+        err.append(abs(eta - r))
+        est.complete(task, r)
+    tail = err[len(err) // 2:]
+    out = {"steps": len(ready), "mean_abs_err_ms": round(statistics.mean(tail) * 1e3, 3),
+           "max_abs_err_ms": round(max(tail) * 1e3, 3), "first_err_ms": round(err[0] * 1e3, 3),
+           "dram_GBps": round(est.bandwidth(binding.TIER_DRAM) / 1e9, 3),
+           "storage_GBps": round(est.bandwidth(binding.TIER_STORAGE) / 1e9, 3)}
+    est.close()
+    return out
+
+
 def block_device(path: str) -> str:
     """Name and kind of the block device holding `path` (from sysfs)."""
     try:
@@ -209,12 +269,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama-2-7b", choices=list(synth.WORKLOADS) + ["stress-8g"])
+    ap.add_argument("--workload", default="llama-2-7b", choices=list(synth.WORKLOADS) + ["stress-8g", "lora-70b-r32"])
     ap.add_argument("--engine", default="kernel", choices=["kernel", "sdma"])
     ap.add_argument("--regime", default="dram", choices=["dram", "ring", "direct"],
                     help="dram: partition cached in the pinned pool (graded); ring: streamed from the file "
                          "through pinned slots (buffered reads); direct: the same with O_DIRECT reads")
     ap.add_argument("--chunk-size", type=int, default=0, help="chunk size in bytes (default: the workload's)")
+    ap.add_argument("--dev-alignment", type=int, default=0,
+                    help="load into a device layout with this alignment (K1-scatter, or copy engine + K2)")
     ap.add_argument("--io-threads", type=int, default=8)
     ap.add_argument("--ring-slots", type=int, default=32)
     ap.add_argument("--dir", default=None, help="where the converted checkpoint lives")
@@ -248,9 +310,11 @@ def main():
     log(f"measured peaks: pinned->HBM copy {h2d_peak} GB/s, HBM copy {hbm_peak} GB/s")
 
     C = args.chunk_size or spec.chunk_size
-    with binding.Checkpoint(d) as probe:
+    with binding.Checkpoint(d, index_only=True, dev_alignment=args.dev_alignment) as probe:
         T = probe.total_bytes
-    n_chunks = -(-T // C)
+    with binding.Checkpoint(d, index_only=True) as probe:
+        T_file = probe.total_bytes
+    n_chunks = -(-T_file // C)
     cached = args.regime == "dram"
     t0 = time.time()
     pool = binding.Pool(C, n_chunks if cached else args.ring_slots)
@@ -261,7 +325,7 @@ def main():
         pool.cache(d, io_threads=args.io_threads)
         fill_s = time.time() - t0
         log(f"DRAM tier filled in {fill_s:.1f} s")
-    open_kw = dict(pool=pool, engine=args.engine)
+    open_kw = dict(pool=pool, engine=args.engine, dev_alignment=args.dev_alignment)
     if not cached:
         open_kw.update(chunk_size=C, io_threads=args.io_threads, ring_slots=args.ring_slots,
                        direct_io=args.regime == "direct")
@@ -308,10 +372,18 @@ def main():
             if got.tobytes() != want.tobytes():
                 raise SystemExit(f"bench: tensor {names[i]} differs from the generator's bytes")
     del views
-    extras = {} if (args.no_extras or not cached) else measure_extras(torch, spec, d, pool, buf, stream, args.engine)
+    extras = ({} if (args.no_extras or not cached or args.dev_alignment) else
+              measure_extras(torch, spec, d, pool, buf, stream, args.engine))
     if fill_s is not None:
         extras["dram_tier_fill"] = {"GBps": round(T / fill_s / 1e9, 3), "s": round(fill_s, 3),
                                     "io_threads": args.io_threads, "source": "converted file, page cache warm"}
+    storage = None
+    if not cached and args.regime == "direct":
+        storage = storage_peak(os.path.join(d, "sllm.part0"))
+        extras["storage_peak"] = storage
+    tiers = binding.TIER_DRAM | (0 if cached else binding.TIER_STORAGE)
+    extras["estimator"] = estimator_replay(ready, T, tiers, (h2d_peak or 50.0) * 1e9,
+                                           (storage["GBps"] if storage else 5.0) * 1e9)
     if not cached:
         extras["ring"] = {"io_threads": args.io_threads, "ring_slots": args.ring_slots,
                           "direct_io": int(last_stats.get("direct_io", 0)),
@@ -325,7 +397,8 @@ def main():
     achieved = T / k_avg_s / 1e9
     value = T * args.steps / elapsed / 1e9
     k1_counters = (profiled_counters("k1_gather_llama-2-7b.md", "kernels.hip")
-                   if cached and args.engine == "kernel" and spec.name == "llama-2-7b" and C == 16 << 20 else None)
+                   if cached and args.engine == "kernel" and spec.name == "llama-2-7b" and C == 16 << 20
+                   and not args.dev_alignment else None)
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -338,9 +411,10 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u8",
-        "data": DATA.get(spec.name.split("-cap")[0], DATA["llama"]),
+        "data": next((v for k, v in DATA.items() if spec.name.startswith(k)), DATA["llama"]),
         "config": {"workload": spec.name, "bytes": T, "tensors": len(spec.tensors), "chunk_size": C,
-                   "alignment": spec.alignment, "engine": args.engine, "regime": REGIME[args.regime]},
+                   "alignment": spec.alignment, "dev_alignment": args.dev_alignment, "engine": args.engine,
+                   "regime": REGIME[args.regime]},
         "time_to_ready_s": round(statistics.median(ready), 5),
         "load_GBps": round(T / statistics.median(loads) / 1e9, 3),
         "roofline": {"bound": "pcie", "achieved": round(achieved, 3), "peak": PCIE_GEN5_X16_GBPS, "unit": "GB/s",
@@ -348,7 +422,8 @@ def main():
                      "traffic": k1_counters["fetch_bytes_per_launch"] if k1_counters else None,
                      "traffic_write": k1_counters["write_bytes_per_launch"] if k1_counters else None,
                      "algorithmic_bytes": T,
-                     "kernel": ("k1_gather" if cached and args.engine == "kernel" else
+                     "kernel": ("k1_gather" if cached and args.engine == "kernel" and not args.dev_alignment else
+                                "k_scatter (host source)" if cached and args.engine == "kernel" else
                                 "whole load on the caller's stream (events around sllm_load)"),
                      "kernel_ms": round(statistics.mean(kernel_ms), 3),
                      "peak_measured": None if h2d_peak is None else round(h2d_peak, 3),

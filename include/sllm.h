@@ -108,6 +108,16 @@ int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* tensor);
 int32_t sllm_writer_close(sllm_writer* w);
 void    sllm_writer_abort(sllm_writer* w);
 
+/* Convert safetensors shards (the format Hugging Face checkpoints ship in)
+ * straight into out_dir: every tensor of every shard, in shard order and,
+ * within a shard, in the order its bytes sit in the file, so each shard is
+ * read front to back once.  Supported dtypes: F32, F16, BF16, I8.
+ * Errors: INVAL (another dtype, more than 8 dimensions, a name repeated
+ * across shards), IO, FORMAT (malformed header, data outside the file,
+ * overlapping tensors, size != numel * itemsize).  On error no files remain. */
+int32_t sllm_convert_safetensors(const char* const* paths, uint64_t n_paths, const char* out_dir,
+                                 const sllm_convert_opts* opts);
+
 /* =========================================================================
  * Pinned host chunk pool: the DRAM tier (Sec. 4.2, chunk-based data
  * management: fixed-size chunks, allocation and eviction under the
@@ -267,8 +277,14 @@ typedef struct sllm_ipc_desc {
     uint64_t offset;            /* start of the buffer inside that allocation      */
     uint64_t bytes;             /* length of the buffer                            */
     int32_t  device;
-    uint32_t reserved;
+    uint32_t flags;             /* SLLM_IPC_*                                      */
 } sllm_ipc_desc;
+
+/* event_handle is valid: the importer's stream waits for it on the device.
+ * Without it the exporter finished the load before filling the descriptor
+ * (the runtime offers no interprocess events), and the importer waits for
+ * nothing. */
+#define SLLM_IPC_HAS_EVENT 1u
 
 /* Largest allocation this library shares across processes: opening handles
  * of larger allocations does not complete on the MI355X systems it was
@@ -282,6 +298,8 @@ typedef struct sllm_import sllm_import;
  * SLLM_IPC_MAX_ALLOCATION bytes) with other processes: fills *desc (plain
  * bytes, safe to send through a pipe or file) and records the handoff event
  * on `stream`, after the work already queued there (typically sllm_load).
+ * Where the runtime has no interprocess events, it instead waits for that
+ * work to finish and leaves SLLM_IPC_HAS_EVENT clear.
  * Keep the export alive while importers use the buffer.
  * Errors: INVAL (not device memory, allocation too large, range outside it), HIP. */
 int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32_t device, void* stream,

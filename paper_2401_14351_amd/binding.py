@@ -67,7 +67,7 @@ class Stats(C.Structure):
 
 class IpcDesc(C.Structure):
     _fields_ = [("mem_handle", C.c_uint8 * 64), ("event_handle", C.c_uint8 * 64), ("offset", C.c_uint64),
-                ("bytes", C.c_uint64), ("device", C.c_int32), ("reserved", C.c_uint32)]
+                ("bytes", C.c_uint64), ("device", C.c_int32), ("flags", C.c_uint32)]
 
 
 # name -> (restype, argtypes); every symbol the header declares
@@ -77,6 +77,8 @@ SIGNATURES = {
     "sllm_writer_add": (C.c_int32, [C.c_void_p, C.POINTER(SrcTensor)]),
     "sllm_writer_close": (C.c_int32, [C.c_void_p]),
     "sllm_writer_abort": (None, [C.c_void_p]),
+    "sllm_convert_safetensors": (C.c_int32, [C.POINTER(C.c_char_p), C.c_uint64, C.c_char_p,
+                                             C.POINTER(ConvertOpts)]),
     "sllm_pool_create": (C.c_int32, [C.c_uint64, C.c_uint64, C.c_int32, C.POINTER(C.c_void_p)]),
     "sllm_pool_destroy": (C.c_int32, [C.c_void_p]),
     "sllm_pool_query": (C.c_int32, [C.c_void_p, C.POINTER(PoolInfo)]),
@@ -221,6 +223,15 @@ def convert_array(tensors: Sequence[Tuple[str, str, Sequence[int], object]], out
     opts = ConvertOpts(alignment, chunk_size, 0, 0)
     os.makedirs(out_dir, exist_ok=True)
     check(L.sllm_convert(arr, len(structs), out_dir.encode(), C.byref(opts)))
+
+
+def convert_safetensors(paths: Sequence[str], out_dir: str, alignment: int = 256,
+                        chunk_size: int = 16 << 20) -> None:
+    """``sllm_convert_safetensors`` over one or more shards."""
+    arr = (C.c_char_p * max(1, len(paths)))(*[p.encode() for p in paths])
+    opts = ConvertOpts(alignment, chunk_size, 0, 0)
+    os.makedirs(out_dir, exist_ok=True)
+    check(lib().sllm_convert_safetensors(arr, len(paths), out_dir.encode(), C.byref(opts)))
 
 
 # ---------------------------------------------------------------------------

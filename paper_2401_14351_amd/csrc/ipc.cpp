@@ -44,18 +44,39 @@ extern "C" int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32
     auto* ex = new (std::nothrow) sllm_export;
     if (!ex) return fail(SLLM_E_NOMEM, "out of host memory");
     ex->device = device;
-    hipError_t e = hipEventCreateWithFlags(&ex->ev, hipEventDisableTiming | hipEventInterprocess);
-    if (e == hipSuccess) e = hipEventRecord(ex->ev, static_cast<hipStream_t>(stream));
-    hipIpcEventHandle_t eh;
-    if (e == hipSuccess) e = hipIpcGetEventHandle(&eh, ex->ev);
-    if (e != hipSuccess) {
-        if (ex->ev) (void)hipEventDestroy(ex->ev);
-        delete ex;
-        return fail(SLLM_E_HIP, "handoff event: %s", hipGetErrorString(e));
-    }
     std::memset(desc, 0, sizeof *desc);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // preferred: an interprocess event the importer's stream waits on
+    hipIpcEventHandle_t eh;
+    const char* what = "hipEventCreateWithFlags(interprocess)";
+    hipError_t e = hipEventCreateWithFlags(&ex->ev, hipEventDisableTiming | hipEventInterprocess);
+    if (e == hipSuccess) {
+        what = "hipIpcGetEventHandle";
+        e = hipIpcGetEventHandle(&eh, ex->ev);
+    }
+    if (e == hipSuccess) {
+        what = "hipEventRecord";
+        e = hipEventRecord(ex->ev, s);
+        if (e != hipSuccess) {
+            (void)hipEventDestroy(ex->ev);
+            delete ex;
+            return fail(SLLM_E_HIP, "%s: %s", what, hipGetErrorString(e));
+        }
+        std::memcpy(desc->event_handle, &eh, sizeof eh);
+        desc->flags |= SLLM_IPC_HAS_EVENT;
+    } else {
+        // no interprocess events here: finish the load before handing out the buffer
+        log_msg(1, "%s failed (%s); the export synchronizes on the host instead", what, hipGetErrorString(e));
+        if (ex->ev) (void)hipEventDestroy(ex->ev);
+        ex->ev = nullptr;
+        (void)hipGetLastError();
+        e = hipStreamSynchronize(s);
+        if (e != hipSuccess) {
+            delete ex;
+            return fail(SLLM_E_HIP, "hipStreamSynchronize: %s", hipGetErrorString(e));
+        }
+    }
     std::memcpy(desc->mem_handle, &mh, sizeof mh);
-    std::memcpy(desc->event_handle, &eh, sizeof eh);
     desc->offset = off;
     desc->bytes = bytes;
     desc->device = device;
@@ -85,14 +106,25 @@ extern "C" int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, voi
     hipIpcEventHandle_t eh;
     std::memcpy(&mh, desc->mem_handle, sizeof mh);
     std::memcpy(&eh, desc->event_handle, sizeof eh);
+    if (desc->flags & ~SLLM_IPC_HAS_EVENT) {
+        delete im;
+        return fail(SLLM_E_INVAL, "unknown descriptor flags 0x%x", desc->flags);
+    }
+    const char* what = "hipIpcOpenMemHandle";
     hipError_t e = hipIpcOpenMemHandle(&im->base, mh, hipIpcMemLazyEnablePeerAccess);
-    if (e == hipSuccess) e = hipIpcOpenEventHandle(&im->ev, eh);
-    if (e == hipSuccess) e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), im->ev, 0);
+    if (e == hipSuccess && (desc->flags & SLLM_IPC_HAS_EVENT)) {
+        what = "hipIpcOpenEventHandle";
+        e = hipIpcOpenEventHandle(&im->ev, eh);
+        if (e == hipSuccess) {
+            what = "hipStreamWaitEvent";
+            e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), im->ev, 0);
+        }
+    }
     if (e != hipSuccess) {
         if (im->ev) (void)hipEventDestroy(im->ev);
         if (im->base) (void)hipIpcCloseMemHandle(im->base);
         delete im;
-        return fail(SLLM_E_HIP, "opening the exported buffer: %s", hipGetErrorString(e));
+        return fail(SLLM_E_HIP, "%s: %s", what, hipGetErrorString(e));
     }
     *dev_ptr = static_cast<uint8_t*>(im->base) + desc->offset;
     *out = im;

@@ -40,7 +40,7 @@ def test_ipc_handoff_opt125m(torch_cuda, tmp_path):
                 torch.cuda._sleep(50_000_000)  # the load is still queued when the consumer starts
             ck.load_into(buf, s)
             ex = binding.Export(buf, s)
-            print("[gpu-ipc] starting the consumer", flush=True)
+            print("[gpu-ipc] starting the consumer; device-side event:", bool(ex.desc.flags & 1), flush=True)
             r = subprocess.run([sys.executable, os.path.join(HERE, "ipc_consumer.py"), d, ex.desc_bytes.hex(),
                                 "opt-125m"], capture_output=True, text=True, timeout=240)
             print(r.stdout, r.stderr[-2000:], flush=True)
