@@ -198,6 +198,96 @@ def estimator_replay(ready, T, tiers, dram_bps, storage_bps):
     return out
 
 
+def ablation(torch, spec, d: str, io_threads: int = 8):
+    """The paper's loading ladder (Sec. 7.2, performance breakdown) rebuilt on
+    this machine: each rung loads the same partition file into one HBM
+    buffer, adding one technique at a time.  Rungs 1-4 are plain host code
+    (pageable buffers, torch copies), rungs 5-6 are this library."""
+    import mmap
+    import threading
+
+    path = os.path.join(d, "sllm.part0")
+    with binding.Checkpoint(d, index_only=True) as ck:
+        tensors, T = ck.tensors(), ck.total_bytes
+    C = spec.chunk_size
+    dev = torch.empty(T, dtype=torch.uint8, device="cuda:0")
+
+    def cold():
+        fd = os.open(path, os.O_RDONLY)
+        os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+        os.close(fd)
+
+    def read_by_tensor():
+        fd = os.open(path, os.O_RDONLY)
+        for t in tensors:
+            b = os.pread(fd, t.nbytes, t.offset)
+            if t.nbytes:
+                dev[t.offset:t.offset + t.nbytes].copy_(torch.frombuffer(bytearray(b), dtype=torch.uint8))
+        os.close(fd)
+
+    def bulk(direct: bool, threads: int):
+        fd = os.open(path, os.O_RDONLY | (os.O_DIRECT if direct else 0))
+        n = -(-T // C)
+        counter = iter(range(n))
+        lock = threading.Lock()
+
+        def worker():
+            buf = mmap.mmap(-1, C)  # page-aligned, pageable
+            host = torch.frombuffer(buf, dtype=torch.uint8)
+            while True:
+                with lock:
+                    k = next(counter, None)
+                if k is None:
+                    return
+                want = min(C, os.fstat(fd).st_size - k * C)
+                got = os.preadv(fd, [memoryview(buf)[:want]], k * C)
+                m = min(C, T - k * C)
+                assert got >= m
+                dev[k * C:k * C + m].copy_(host[:m])
+        ts = [threading.Thread(target=worker) for _ in range(threads)]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        os.close(fd)
+
+    def pinned_sequential():
+        with binding.Pool(C, -(-T // C)) as pool:
+            pool.cache(d, io_threads=io_threads, direct_io=True)
+            with binding.Checkpoint(d, pool=pool) as ck:
+                ck.load_into(dev)
+                torch.cuda.synchronize()
+            pool.evict(d)
+
+    def pipeline():
+        with binding.Pool(C, 4 * io_threads) as pool:
+            with binding.Checkpoint(d, pool=pool, direct_io=True, io_threads=io_threads,
+                                    ring_slots=4 * io_threads) as ck:
+                ck.load_into(dev)
+                torch.cuda.synchronize()
+
+    rungs = [("ReadByTensor", True, read_by_tensor), ("+bulk", True, lambda: bulk(False, 1)),
+             ("+direct I/O", False, lambda: bulk(True, 1)),
+             (f"+{io_threads} I/O threads", False, lambda: bulk(True, io_threads)),
+             ("+pinned chunk pool (tiers in sequence)", False, pinned_sequential),
+             ("+pipeline (streamed ring)", False, pipeline)]
+    out, prev = [], None
+    for name, needs_cold, fn in rungs:
+        if needs_cold:
+            cold()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        gbps = T / dt / 1e9
+        out.append({"rung": name, "s": round(dt, 3), "GBps": round(gbps, 3),
+                    "step_gain": None if prev is None else round(gbps / prev, 2)})
+        prev = gbps
+        log("ablation", out[-1])
+    return out
+
+
 def block_device(path: str) -> str:
     """Name and kind of the block device holding `path` (from sysfs)."""
     try:
@@ -286,6 +376,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the copy-engine, repack and cold direct-read measurements")
     ap.add_argument("--no-verify", action="store_true", help="skip the sampled parity check")
+    ap.add_argument("--ablation", action="store_true",
+                    help="run the paper's loading ladder (per-tensor reads ... pipeline) on the file instead")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with one 1 GiB HBM->HBM copy (the counter calibration kernel)")
     args = ap.parse_args()
@@ -305,6 +397,13 @@ def main():
     import torch
 
     torch.cuda.init()
+    if args.ablation:
+        ladder = ablation(torch, spec, d, args.io_threads)
+        base = ladder[0]["GBps"]
+        print(json.dumps({"ablation": ladder, "workload": spec.name, "device": block_device(d),
+                          "storage_peak": storage_peak(os.path.join(d, "sllm.part0")),
+                          "total_gain": round(ladder[-1]["GBps"] / base, 2)}), flush=True)
+        return
     stream = torch.cuda.Stream()
     h2d_peak, hbm_peak = (None, None) if args.no_peaks else measure_peaks(torch)
     log(f"measured peaks: pinned->HBM copy {h2d_peak} GB/s, HBM copy {hbm_peak} GB/s")

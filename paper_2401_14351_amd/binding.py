@@ -405,7 +405,10 @@ class Export:
     """Share a loaded uint8 device buffer with another process (``sllm_export_*``).
 
     The handoff event is recorded on ``stream`` after the work queued there,
-    so export right after ``Checkpoint.load_into(buf, stream)``."""
+    so export right after ``Checkpoint.load_into(buf, stream)``.  The whole
+    device allocation holding ``buf`` is shared, so give the buffer its own
+    allocation (a block of torch's caching allocator may sit inside a segment
+    larger than ``SLLM_IPC_MAX_ALLOCATION``)."""
 
     def __init__(self, buf, stream=None, device: int = 0):
         self.desc = IpcDesc()

@@ -33,6 +33,10 @@ struct GatherArgs {
     uint64_t first_chunk;
     uint32_t tiles_per_chunk;
     uint32_t n_tiles;
+    // a batch of chunks from separate slots, passed inline (batch_n > 0)
+    uint32_t batch_n;
+    const uint8_t* batch_src[kGatherBatch];
+    uint64_t batch_chunk[kGatherBatch];
 };
 
 template <bool NT>
@@ -63,10 +67,11 @@ __global__ __launch_bounds__(kThreads) void k1_gather(GatherArgs a) {
     for (uint32_t t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
         const uint32_t c = t / a.tiles_per_chunk;
         const uint32_t j = t - c * a.tiles_per_chunk;
-        const uint64_t base = (a.first_chunk + c) * a.chunk;
+        const uint64_t k = a.batch_n ? a.batch_chunk[c] : a.first_chunk + c;
+        const uint64_t base = k * a.chunk;
         if (base >= a.total) continue;
         const uint64_t len = a.total - base < a.chunk ? a.total - base : a.chunk;
-        const uint8_t* src = a.table ? a.table[c] : a.single;
+        const uint8_t* src = a.batch_n ? a.batch_src[c] : a.table ? a.table[c] : a.single;
         uint8_t* dst = a.dst + base;
         const uint64_t lo = (uint64_t)j * kTile + threadIdx.x * kVec;
         u32x4 v[U];
@@ -121,13 +126,76 @@ GatherShape gather_shape() {
     return s;
 }
 
+namespace {
+
+int32_t launch_tiles(GatherArgs a, uint64_t tpc, uint64_t n_chunks, const GatherShape& sh, hipStream_t stream) {
+    a.tiles_per_chunk = (uint32_t)tpc;
+    a.n_tiles = (uint32_t)(n_chunks * tpc);
+    const uint32_t grid = a.n_tiles < sh.blocks ? a.n_tiles : sh.blocks;
+    const dim3 gd(grid), bd(kThreads);
+    switch (sh.unroll * 2 + (sh.nontemporal ? 1 : 0)) {
+        case 2: k1_gather<1, false><<<gd, bd, 0, stream>>>(a); break;
+        case 3: k1_gather<1, true><<<gd, bd, 0, stream>>>(a); break;
+        case 4: k1_gather<2, false><<<gd, bd, 0, stream>>>(a); break;
+        case 5: k1_gather<2, true><<<gd, bd, 0, stream>>>(a); break;
+        case 8: k1_gather<4, false><<<gd, bd, 0, stream>>>(a); break;
+        default: k1_gather<4, true><<<gd, bd, 0, stream>>>(a); break;
+    }
+    SLLM_HIP(hipGetLastError());
+    return SLLM_OK;
+}
+
+}  // namespace
+
+int32_t launch_gather_batch(uint8_t* dst, const uint8_t* const* srcs, const uint64_t* chunks, uint32_t n,
+                            uint64_t chunk, uint64_t total, hipStream_t stream) {
+    if (n == 0) return SLLM_OK;
+    if (n > kGatherBatch || chunk == 0) return fail(SLLM_E_INVAL, "gather batch: bad size");
+    const uint64_t n_all = ceil_div(total, chunk);
+    for (uint32_t i = 0; i < n; ++i)
+        if (chunks[i] >= n_all) return fail(SLLM_E_INVAL, "gather batch: chunk past the end of the image");
+    const bool vec = (chunk % kVec) == 0 && (reinterpret_cast<uintptr_t>(dst) % kVec) == 0;
+    if (!vec) {  // byte geometry: one launch per chunk
+        for (uint32_t i = 0; i < n; ++i) {
+            GatherLaunch g;
+            g.dst = dst;
+            g.single = srcs[i];
+            g.chunk = chunk;
+            g.total = total;
+            g.first_chunk = chunks[i];
+            g.n_chunks = 1;
+            SLLM_TRY(launch_gather(g, stream));
+        }
+        return SLLM_OK;
+    }
+    const GatherShape sh = gather_shape();
+    GatherArgs a{};
+    a.dst = dst;
+    a.chunk = chunk;
+    a.total = total;
+    a.batch_n = n;
+    for (uint32_t i = 0; i < n; ++i) {
+        a.batch_src[i] = srcs[i];
+        a.batch_chunk[i] = chunks[i];
+    }
+    const uint64_t tpc = ceil_div(chunk, (uint64_t)kThreads * kVec * sh.unroll);
+    if (tpc * n >= (1ull << 31)) return fail(SLLM_E_INVAL, "gather batch: chunk size too large");
+    return launch_tiles(a, tpc, n, sh, stream);
+}
+
 int32_t launch_gather(const GatherLaunch& g, hipStream_t stream) {
     if (g.n_chunks == 0 || g.first_chunk * g.chunk >= g.total) return SLLM_OK;
     if (!g.table && g.n_chunks != 1) return fail(SLLM_E_INVAL, "gather: a single slot serves one chunk");
     if (g.chunk == 0 || g.n_chunks > ceil_div(g.total, g.chunk) - g.first_chunk)
         return fail(SLLM_E_INVAL, "gather: chunks past the end of the image");
     const GatherShape sh = gather_shape();
-    GatherArgs a{g.dst, g.table, g.single, g.chunk, g.total, g.first_chunk, 0, 0};
+    GatherArgs a{};
+    a.dst = g.dst;
+    a.table = g.table;
+    a.single = g.single;
+    a.chunk = g.chunk;
+    a.total = g.total;
+    a.first_chunk = g.first_chunk;
     const bool vec = (g.chunk % kVec) == 0 && (reinterpret_cast<uintptr_t>(g.dst) % kVec) == 0;
     if (!vec) {
         uint64_t bytes = g.n_chunks * g.chunk;
@@ -146,19 +214,7 @@ int32_t launch_gather(const GatherLaunch& g, hipStream_t stream) {
         const uint64_t nc = g.n_chunks - c0 < max_chunks ? g.n_chunks - c0 : max_chunks;
         a.table = g.table ? g.table + c0 : nullptr;
         a.first_chunk = g.first_chunk + c0;
-        a.tiles_per_chunk = (uint32_t)tpc;
-        a.n_tiles = (uint32_t)(nc * tpc);
-        const uint32_t grid = a.n_tiles < sh.blocks ? a.n_tiles : sh.blocks;
-        const dim3 gd(grid), bd(kThreads);
-        switch (sh.unroll * 2 + (sh.nontemporal ? 1 : 0)) {
-            case 2: k1_gather<1, false><<<gd, bd, 0, stream>>>(a); break;
-            case 3: k1_gather<1, true><<<gd, bd, 0, stream>>>(a); break;
-            case 4: k1_gather<2, false><<<gd, bd, 0, stream>>>(a); break;
-            case 5: k1_gather<2, true><<<gd, bd, 0, stream>>>(a); break;
-            case 8: k1_gather<4, false><<<gd, bd, 0, stream>>>(a); break;
-            default: k1_gather<4, true><<<gd, bd, 0, stream>>>(a); break;
-        }
-        SLLM_HIP(hipGetLastError());
+        SLLM_TRY(launch_tiles(a, tpc, nc, sh, stream));
     }
     return SLLM_OK;
 }

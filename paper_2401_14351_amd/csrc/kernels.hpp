@@ -24,6 +24,14 @@ struct GatherLaunch {
 };
 int32_t launch_gather(const GatherLaunch& g, hipStream_t stream);
 
+// Up to this many chunks, each from its own slot, in one gather launch.
+constexpr uint32_t kGatherBatch = 16;
+
+// Gather n (<= kGatherBatch) chunks: chunk chunks[i] of the partition from
+// the device-visible slot srcs[i] into dst + chunks[i] * C.
+int32_t launch_gather_batch(uint8_t* dst, const uint8_t* const* srcs, const uint64_t* chunks, uint32_t n,
+                            uint64_t chunk, uint64_t total, hipStream_t stream);
+
 // Kernel launch shape knobs, read from the environment at every launch:
 // SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT.
 struct GatherShape {

@@ -161,6 +161,20 @@ __device__ __forceinline__ uint64_t owner_global(const uint64_t* d, uint64_t lo,
     return lo;
 }
 
+// the same, searching forward from `from` (d[from] <= y): gallop 1, 2, 4 ...
+// entries ahead, then bisect the last step; one load when y is still in the
+// slot of tensor `from`, as it is for most tiles of a large tensor
+__device__ __forceinline__ uint64_t owner_from(const uint64_t* d, uint64_t from, uint64_t last, uint64_t y) {
+    uint64_t lo = from, step = 1;
+    while (lo < last) {
+        const uint64_t probe = last - lo < step ? last : lo + step;
+        if (d[probe] > y) return owner_global(d, lo, probe - 1, y);
+        lo = probe;
+        step <<= 1;
+    }
+    return lo;
+}
+
 template <bool NT>
 __device__ __forceinline__ void st16(uint8_t* p, u32x4 v) {
     if constexpr (NT) {
@@ -178,14 +192,21 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
     __shared__ uint64_t s_dev[kLdsEntries], s_off[kLdsEntries], s_size[kLdsEntries];
     __shared__ uint64_t s_lo, s_hi;
     const Src src{a};
-    for (uint64_t t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
+    // each workgroup walks a contiguous span of tiles, so the owning tensor
+    // of the next tile is found by searching forward from the last one
+    const uint64_t per_block = (a.n_tiles + gridDim.x - 1) / gridDim.x;
+    const uint64_t t_begin = (uint64_t)blockIdx.x * per_block;
+    const uint64_t t_end = t_begin + per_block < a.n_tiles ? t_begin + per_block : a.n_tiles;
+    uint64_t cursor = 0;  // thread 0: owner of the previous tile's last byte
+    for (uint64_t t = t_begin; t < t_end; ++t) {
         const uint64_t yt = (a.tile0 + t) * kTileU;
         const uint64_t lo = yt > a.y0 ? yt : a.y0;
         const uint64_t hi = yt + kTileU < a.y1 ? yt + kTileU : a.y1;
         if (threadIdx.x == 0) {
-            const uint64_t i_lo = owner_global(a.dev, 0, a.n - 1, lo);
+            const uint64_t i_lo = t == t_begin ? owner_global(a.dev, 0, a.n - 1, lo) : owner_from(a.dev, cursor, a.n - 1, lo);
+            cursor = owner_from(a.dev, i_lo, a.n - 1, hi - 1);
             s_lo = i_lo;
-            s_hi = owner_global(a.dev, i_lo, a.n - 1, hi - 1);
+            s_hi = cursor;
         }
         __syncthreads();
         const uint64_t i_lo = s_lo, cnt = s_hi - s_lo + 1;

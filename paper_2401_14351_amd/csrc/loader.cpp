@@ -163,27 +163,27 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         return launch_gather(g, user);
     }
     SLLM_TRY(fork_streams(h, user));
-    const uint64_t max_copy = std::max(sdma_max_copy(), C);
+    // merge chunks that are adjacent in host memory into one copy; with a
+    // device layout a merged run goes to this stream's HBM staging chunk and
+    // one scatter launch repacks it
+    const uint64_t max_copy = h->dev_align ? h->layout.staging_stride : std::max(sdma_max_copy(), C);
     uint64_t issued = 0;
     for (uint64_t k = 0; k < n;) {
-        // merge chunks that are adjacent in host memory into one copy
         uint64_t j = k + 1;
         while (j < n && p->stride == C && p->host[e->chunks[j]] == p->host[e->chunks[j - 1]] + C &&
                (j + 1 - k) * C <= max_copy)
             ++j;
         const uint64_t x0 = k * C, x1 = std::min(j * C, T);
         const uint32_t si = (uint32_t)(issued % h->streams.size());
+        hipStream_t s = h->streams[si];
         if (h->dev_align) {
-            for (uint64_t q = k; q < j; ++q) {
-                const uint64_t a = q * C, b = std::min(a + C, T);
-                SLLM_TRY(move_chunk(h, dst, q, p->host[e->chunks[q]], p->mapped[e->chunks[q]], b - a,
-                                    (uint32_t)((issued + q - k) % h->streams.size()), h->streams[(issued + q - k) % h->streams.size()]));
-            }
-            issued += j - k;
+            uint8_t* stage = h->layout.staging + (uint64_t)si * h->layout.staging_stride;
+            SLLM_HIP(hipMemcpyAsync(stage, p->host[e->chunks[k]], x1 - x0, hipMemcpyHostToDevice, s));
+            SLLM_TRY(launch_scatter_window(h->layout, dst, stage, x0, x1, /*src_is_host=*/false, s));
         } else {
-            SLLM_HIP(hipMemcpyAsync(dst + x0, p->host[e->chunks[k]], x1 - x0, hipMemcpyHostToDevice, h->streams[si]));
-            ++issued;
+            SLLM_HIP(hipMemcpyAsync(dst + x0, p->host[e->chunks[k]], x1 - x0, hipMemcpyHostToDevice, s));
         }
+        ++issued;
         k = j;
     }
     h->stats.n_launches = issued;
@@ -260,36 +260,58 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     threads.reserve(nt);
     for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader);
 
+    // kernel loads in the file layout move every chunk that is ready in one
+    // batched gather; the other paths move one chunk per call
+    const uint32_t max_batch = (h->engine == SLLM_ENGINE_KERNEL && !h->dev_align) ? kGatherBatch : 1;
+    std::vector<std::pair<uint64_t, uint32_t>> batch;
+    batch.reserve(max_batch);
     double wait_s = 0;
-    for (uint64_t i = 0; i < n; ++i) {
-        std::pair<uint64_t, uint32_t> item;
+    uint64_t moved = 0, launches = 0;
+    while (moved < n) {
+        batch.clear();
         {
             const double w0 = now_s();
             std::unique_lock<std::mutex> lk(mu);
             cv_ready.wait(lk, [&] { return stop || !ready_q.empty(); });
             wait_s += now_s() - w0;
             if (ready_q.empty()) break;  // stopped by a reader's error
-            item = ready_q.front();
-            ready_q.pop_front();
+            while (!ready_q.empty() && batch.size() < max_batch) {
+                batch.push_back(ready_q.front());
+                ready_q.pop_front();
+            }
         }
-        const uint64_t k = item.first;
-        Slot& s = h->slots[item.second];
-        const uint32_t si = (uint32_t)(i % h->streams.size());
+        const uint32_t si = (uint32_t)(launches % h->streams.size());
         hipStream_t st = h->streams[si];
-        int32_t rc = move_chunk(h, dst, k, s.host, s.mapped, std::min(C, T - k * C), si, st);
-        if (rc == SLLM_OK) {
-            hipError_t e = hipEventRecord(s.done, st);
+        int32_t rc;
+        if (max_batch > 1) {
+            const uint8_t* srcs[kGatherBatch];
+            uint64_t ks[kGatherBatch];
+            for (size_t b = 0; b < batch.size(); ++b) {
+                srcs[b] = h->slots[batch[b].second].mapped;
+                ks[b] = batch[b].first;
+            }
+            rc = launch_gather_batch(dst, srcs, ks, (uint32_t)batch.size(), C, T, st);
+        } else {
+            const uint64_t k = batch[0].first;
+            const Slot& s0 = h->slots[batch[0].second];
+            rc = move_chunk(h, dst, k, s0.host, s0.mapped, std::min(C, T - k * C), si, st);
+        }
+        for (size_t b = 0; rc == SLLM_OK && b < batch.size(); ++b) {
+            hipError_t e = hipEventRecord(h->slots[batch[b].second].done, st);
             if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
         }
+        ++launches;
         std::lock_guard<std::mutex> g(mu);
-        if (rc != SLLM_OK) {
+        for (const auto& item : batch) {
+            if (rc == SLLM_OK) h->slots[item.second].pending = true;
             free_q.push_back(item.second);
+        }
+        if (rc != SLLM_OK) {
             set_error(rc);
             break;
         }
-        s.pending = true;
-        free_q.push_back(item.second);
-        cv_free.notify_one();
+        moved += batch.size();
+        cv_free.notify_all();
     }
     {
         std::lock_guard<std::mutex> g(mu);
@@ -300,7 +322,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     h->stats.read_wait_s = wait_s;
     h->stats.bytes_read = bytes_read;
     h->stats.bytes_bounced = bytes_bounced;
-    h->stats.n_launches = n;
+    h->stats.n_launches = launches;
     if (err != SLLM_OK) {
         for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);  // drain in-flight copies
         return fail(err, "%s", err_msg.c_str());
@@ -447,9 +469,12 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
             file_off[i] = h->ix.tensors[i].offset;
             sizes[i] = h->ix.tensors[i].nbytes;
         }
+        // copy-engine loads stage in HBM: one chunk per stream when streaming,
+        // merged runs of up to 64 MiB when the partition is cached
         const uint64_t staging = (h->engine == SLLM_ENGINE_SDMA) ? h->n_streams : 0;
+        const uint64_t stage_bytes = h->cached ? std::max<uint64_t>(h->chunk, 64ull << 20) : h->chunk;
         st = device_layout_build(file_off, sizes, h->dev_off, h->ix.total, h->dev_total, h->dev_align, staging,
-                                 h->chunk, &h->layout);
+                                 stage_bytes, &h->layout);
         if (st != SLLM_OK) return bail(st);
     }
     h->stats.io_threads = h->io_threads;

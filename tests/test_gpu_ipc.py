@@ -34,6 +34,10 @@ def test_ipc_handoff_opt125m(torch_cuda, tmp_path):
     with binding.Pool(spec.chunk_size, 16) as pool:
         pool.cache(d)
         with binding.Checkpoint(d, pool=pool) as ck:
+            # the shared buffer must be its own (small) allocation, not a block
+            # carved from a large segment the caching allocator kept around
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
             buf = torch.empty(ck.total_bytes, dtype=torch.uint8, device="cuda:0")
             s = torch.cuda.Stream()
             with torch.cuda.stream(s):

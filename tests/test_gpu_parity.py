@@ -362,3 +362,22 @@ def test_gather_shapes(torch_cuda, opt125m, shape, monkeypatch):
         pool.evict(d)
     with binding.Checkpoint(d, chunk_size=3 << 20) as ck:
         assert_same(run_load(torch, ck, len(want)), want, f"streamed {shape}")
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("C", [64 << 10, (64 << 10) + 48, 1 << 20])
+def test_streamed_batches(torch_cuda, opt125m, engine, C):
+    """Many small chunks through a deep ring: the issue loop moves every
+    ready chunk of a pass in one batched gather (up to 16 slots)."""
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, _ = expected(tensors, spec.alignment)
+    with binding.Checkpoint(d, engine=engine, chunk_size=C, ring_slots=48, io_threads=8) as ck:
+        for rep in range(2):
+            assert_same(run_load(torch, ck, len(want)), want, f"C={C} rep {rep}")
+        st = ck.stats()
+        n = -(-len(want) // C)
+        assert st["n_chunks"] == n
+        if engine == "kernel" and C % 16 == 0:
+            assert st["n_launches"] <= n
+        say("batches", engine, C, "chunks", n, "launches", st["n_launches"])
