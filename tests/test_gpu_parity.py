@@ -381,3 +381,41 @@ def test_streamed_batches(torch_cuda, opt125m, engine, C):
         if engine == "kernel" and C % 16 == 0:
             assert st["n_launches"] <= n
         say("batches", engine, C, "chunks", n, "launches", st["n_launches"])
+
+
+def test_concurrent_handles(torch_cuda, opt125m):
+    """Handles are independent: two threads load through separate handles
+    (one pool cache, separate streams) and a third streams from the file."""
+    import threading
+
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, _ = expected(tensors, spec.alignment)
+    errors, results = [], {}
+    with binding.Pool(spec.chunk_size, 16 + 8) as pool:
+        pool.cache(d)
+
+        def work(tag, **kw):
+            try:
+                s = torch.cuda.Stream()
+                with binding.Checkpoint(d, **kw) as ck:
+                    for rep in range(3):
+                        buf = torch.empty(len(want), dtype=torch.uint8, device="cuda:0")
+                        ck.load_into(buf, s)
+                        s.synchronize()
+                        results[(tag, rep)] = buf.cpu().numpy().tobytes()
+            except Exception as e:  # noqa: BLE001
+                errors.append(e)
+
+        ts = [threading.Thread(target=work, args=("k1",), kwargs=dict(pool=pool)),
+              threading.Thread(target=work, args=("sdma",), kwargs=dict(pool=pool, engine="sdma")),
+              threading.Thread(target=work, args=("ring",), kwargs=dict(chunk_size=4 << 20))]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        pool.evict(d)
+    assert not errors, errors
+    assert len(results) == 9
+    for k, v in results.items():
+        assert_same(v, want, str(k))

@@ -285,3 +285,14 @@ def test_index_only_open_matches_oracle_layout(L, tmp_path, A, A2):
         with pytest.raises(binding.SllmError) as ei:
             ck.load(0, 1 << 30)
         assert ei.value.code == -1
+
+
+@pytest.mark.skipif(not os.path.exists("/dev/full"), reason="no /dev/full")
+def test_convert_reports_a_full_disk(L, tmp_path):
+    """A write error (ENOSPC) ends the conversion with SLLM_E_IO and no files."""
+    os.symlink("/dev/full", tmp_path / "sllm.part0")
+    big = np.zeros(16 << 20, dtype=np.uint8)  # larger than the writer's staging buffer
+    with pytest.raises(binding.SllmError) as ei:
+        binding.convert([("w", "i8", (big.size,), big)], str(tmp_path), 256, 1 << 20)
+    assert ei.value.code == -2 and "write" in ei.value.message
+    assert not os.path.exists(tmp_path / "sllm.index")
