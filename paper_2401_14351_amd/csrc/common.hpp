@@ -5,6 +5,8 @@
 #include <chrono>
 #include <cstdarg>
 #include <cstdint>
+#include <exception>
+#include <new>
 #include <string>
 
 #include "sllm.h"
@@ -41,6 +43,19 @@ int log_level();
 void log_msg(int level, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 }  // namespace sllm
+
+// Closes the function-try-block of an extern "C" entry point that returns a
+// status: no C++ exception crosses the C ABI.
+#define SLLM_CATCH_ALL                                                          \
+    catch (const std::bad_alloc&) {                                             \
+        return ::sllm::fail(SLLM_E_NOMEM, "out of host memory");                \
+    }                                                                           \
+    catch (const std::exception& sllm_exc_) {                                   \
+        return ::sllm::fail(SLLM_E_INVAL, "unexpected error: %s", sllm_exc_.what()); \
+    }                                                                           \
+    catch (...) {                                                               \
+        return ::sllm::fail(SLLM_E_INVAL, "unexpected error");                  \
+    }
 
 // Evaluate a status-returning expression and return its status on failure.
 #define SLLM_TRY(expr)                      \

@@ -41,7 +41,7 @@ double queued_s(const sllm_estimator* e) {
 
 }  // namespace
 
-extern "C" int32_t sllm_estimator_create(double dram_bps, double storage_bps, double weight, sllm_estimator** out) {
+extern "C" int32_t sllm_estimator_create(double dram_bps, double storage_bps, double weight, sllm_estimator** out) try {
     clear_error();
     if (!out) return fail(SLLM_E_INVAL, "out is NULL");
     *out = nullptr;
@@ -55,21 +55,21 @@ extern "C" int32_t sllm_estimator_create(double dram_bps, double storage_bps, do
     e->weight = weight;
     *out = e;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
 extern "C" void sllm_estimator_destroy(sllm_estimator* e) { delete e; }
 
-extern "C" int32_t sllm_estimator_query(const sllm_estimator* e, uint64_t bytes, uint32_t tiers, double* eta_s) {
+extern "C" int32_t sllm_estimator_query(const sllm_estimator* e, uint64_t bytes, uint32_t tiers, double* eta_s) try {
     clear_error();
     if (!e || !eta_s) return fail(SLLM_E_INVAL, "estimator and eta_s must be non-NULL");
     if (!tiers_ok(tiers)) return fail(SLLM_E_INVAL, "unknown tiers 0x%x", tiers);
     std::lock_guard<std::mutex> g(e->mu);
     *eta_s = queued_s(e) + (double)bytes / e->bw[slowest(e, tiers)];
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_estimator_enqueue(sllm_estimator* e, uint64_t bytes, uint32_t tiers, uint64_t* task,
-                                          double* eta_s) {
+                                          double* eta_s) try {
     clear_error();
     if (!e || !task || !eta_s) return fail(SLLM_E_INVAL, "estimator, task and eta_s must be non-NULL");
     if (!tiers_ok(tiers)) return fail(SLLM_E_INVAL, "unknown tiers 0x%x", tiers);
@@ -79,9 +79,9 @@ extern "C" int32_t sllm_estimator_enqueue(sllm_estimator* e, uint64_t bytes, uin
     *task = e->next_id++;
     e->queue.push_back({*task, bytes, tiers, cost});
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, double seconds) {
+extern "C" int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, double seconds) try {
     clear_error();
     if (!e) return fail(SLLM_E_INVAL, "estimator is NULL");
     if (!(seconds > 0) || !std::isfinite(seconds)) return fail(SLLM_E_INVAL, "seconds must be positive");
@@ -95,13 +95,13 @@ extern "C" int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, dou
         return SLLM_OK;
     }
     return fail(SLLM_E_NOTFOUND, "no queued task %llu", (unsigned long long)task);
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bps) {
+extern "C" int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bps) try {
     clear_error();
     if (!e || !bps) return fail(SLLM_E_INVAL, "estimator and out must be non-NULL");
     if (tier != SLLM_TIER_DRAM && tier != SLLM_TIER_STORAGE) return fail(SLLM_E_INVAL, "unknown tier %u", tier);
     std::lock_guard<std::mutex> g(e->mu);
     *bps = e->bw[tier == SLLM_TIER_DRAM ? 0 : 1];
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL

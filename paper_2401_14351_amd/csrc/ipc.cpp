@@ -24,7 +24,7 @@ struct sllm_import {
 };
 
 extern "C" int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32_t device, void* stream,
-                                      sllm_ipc_desc* desc, sllm_export** out) {
+                                      sllm_ipc_desc* desc, sllm_export** out) try {
     clear_error();
     if (!dev_ptr || !desc || !out) return fail(SLLM_E_INVAL, "dev_ptr, desc and out must be non-NULL");
     *out = nullptr;
@@ -82,18 +82,18 @@ extern "C" int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32
     desc->device = device;
     *out = ex;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_export_destroy(sllm_export* ex) {
+extern "C" int32_t sllm_export_destroy(sllm_export* ex) try {
     clear_error();
     if (!ex) return SLLM_OK;
     DeviceGuard guard(ex->device);
     if (ex->ev) (void)hipEventDestroy(ex->ev);
     delete ex;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, void** dev_ptr, sllm_import** out) {
+extern "C" int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, void** dev_ptr, sllm_import** out) try {
     clear_error();
     if (!desc || !dev_ptr || !out) return fail(SLLM_E_INVAL, "desc, dev_ptr and out must be non-NULL");
     *out = nullptr;
@@ -129,9 +129,9 @@ extern "C" int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, voi
     *dev_ptr = static_cast<uint8_t*>(im->base) + desc->offset;
     *out = im;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_import_close(sllm_import* im) {
+extern "C" int32_t sllm_import_close(sllm_import* im) try {
     clear_error();
     if (!im) return SLLM_OK;
     DeviceGuard guard(im->device);
@@ -140,4 +140,4 @@ extern "C" int32_t sllm_import_close(sllm_import* im) {
     delete im;
     if (e != hipSuccess) return fail(SLLM_E_HIP, "hipIpcCloseMemHandle: %s", hipGetErrorString(e));
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL

@@ -122,10 +122,10 @@ class Parser {
                 case 'r': out->push_back('\r'); break;
                 case 't': out->push_back('\t'); break;
                 case 'u': {
-                    uint32_t c1;
+                    uint32_t c1 = 0;
                     if (!hex4(&c1)) return false;
                     if (c1 >= 0xD800 && c1 < 0xDC00) {  // surrogate pair
-                        uint32_t c2;
+                        uint32_t c2 = 0;
                         if (n_ - i_ < 2 || p_[i_] != '\\' || p_[i_ + 1] != 'u') return err("lone surrogate");
                         i_ += 2;
                         if (!hex4(&c2) || c2 < 0xDC00 || c2 >= 0xE000) return err("bad surrogate pair");

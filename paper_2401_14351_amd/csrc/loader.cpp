@@ -257,8 +257,19 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
 
     const uint32_t nt = (uint32_t)std::min<uint64_t>(h->io_threads, n);
     std::vector<std::thread> threads;
-    threads.reserve(nt);
-    for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader);
+    try {
+        threads.reserve(nt);
+        for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader);
+    } catch (...) {  // could not start every reader: stop the ones that run
+        {
+            std::lock_guard<std::mutex> g(mu);
+            stop = true;
+            cv_free.notify_all();
+        }
+        for (auto& t : threads) t.join();
+        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
+        return fail(SLLM_E_NOMEM, "cannot start %u I/O threads", nt);
+    }
 
     // kernel loads in the file layout move every chunk that is ready in one
     // batched gather; the other paths move one chunk per call
@@ -332,7 +343,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
 
 }  // namespace
 
-extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out) {
+extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out) try {
     clear_error();
     const double t0 = now_s();
     if (!dir || !out) return fail(SLLM_E_INVAL, "dir and out must be non-NULL");
@@ -484,11 +495,11 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
     h->stats.open_s = now_s() - t0;
     *out = h;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
 extern "C" uint64_t sllm_total_bytes(const sllm_ckpt* h) { return h ? h->dev_total : 0; }
 
-extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream) {
+extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream) try {
     clear_error();
     if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
     if (h->busy.exchange(true)) return fail(SLLM_E_BUSY, "a load is already running on this handle");
@@ -530,10 +541,10 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
     h->stats.bytes_loaded = h->dev_total;
     h->stats.load_s = now_s() - t0;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes, void* dst_dev,
-                               uint64_t dst_bytes, void* stream) {
+                               uint64_t dst_bytes, void* stream) try {
     clear_error();
     if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
     if (!h->dev_align) return fail(SLLM_E_INVAL, "the handle was opened without a device alignment");
@@ -553,7 +564,7 @@ extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t
     uint8_t* dst = static_cast<uint8_t*>(dst_dev);
     return launch_scatter_window(h->layout, dst, static_cast<const uint8_t*>(src_dev), 0, h->ix.total,
                                  /*src_is_host=*/false, s);
-}
+} SLLM_CATCH_ALL
 
 namespace {
 
@@ -570,7 +581,7 @@ void fill_info(const sllm_ckpt* h, uint32_t i, sllm_tensor_info* out) {
 
 }  // namespace
 
-extern "C" int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, uint64_t cap, uint64_t* n_total) {
+extern "C" int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, uint64_t cap, uint64_t* n_total) try {
     clear_error();
     if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
     if (cap && !out) return fail(SLLM_E_INVAL, "out is NULL");
@@ -578,18 +589,18 @@ extern "C" int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, 
     if (n_total) *n_total = n;
     for (uint64_t i = 0; i < std::min(cap, n); ++i) fill_info(h, (uint32_t)i, &out[i]);
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_tensor_info* out) {
+extern "C" int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_tensor_info* out) try {
     clear_error();
     if (!h || !name || !out) return fail(SLLM_E_INVAL, "handle, name and out must be non-NULL");
     auto it = h->by_name.find(name);
     if (it == h->by_name.end()) return fail(SLLM_E_NOTFOUND, "no tensor named '%s'", name);
     fill_info(h, it->second, out);
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_get_stats(const sllm_ckpt* hc, sllm_stats* out) {
+extern "C" int32_t sllm_get_stats(const sllm_ckpt* hc, sllm_stats* out) try {
     clear_error();
     if (!hc || !out) return fail(SLLM_E_INVAL, "handle and out must be non-NULL");
     auto* h = const_cast<sllm_ckpt*>(hc);
@@ -602,12 +613,12 @@ extern "C" int32_t sllm_get_stats(const sllm_ckpt* hc, sllm_stats* out) {
     }
     *out = h->stats;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_close(sllm_ckpt* h) {
+extern "C" int32_t sllm_close(sllm_ckpt* h) try {
     clear_error();
     if (!h) return SLLM_OK;
     if (h->busy.load()) return fail(SLLM_E_BUSY, "a load is running on this handle");
     release(h);
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL

@@ -99,7 +99,10 @@ int32_t parallel_chunks(uint64_t n, uint32_t threads, int device, const std::fun
     };
     uint32_t nt = (uint32_t)std::min<uint64_t>(threads ? threads : 1, n ? n : 1);
     std::vector<std::thread> pool;
-    for (uint32_t i = 1; i < nt; ++i) pool.emplace_back(worker);
+    try {
+        for (uint32_t i = 1; i < nt; ++i) pool.emplace_back(worker);
+    } catch (...) {  // fewer threads than asked: the ones running finish the work
+    }
     worker();
     for (auto& t : pool) t.join();
     if (status.load() != SLLM_OK) return fail(status.load(), "%s", msg.c_str());
@@ -130,7 +133,7 @@ std::string canonical(const char* dir) {
 
 }  // namespace
 
-extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int32_t device, sllm_pool** out) {
+extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int32_t device, sllm_pool** out) try {
     clear_error();
     if (!out) return fail(SLLM_E_INVAL, "out is NULL");
     *out = nullptr;
@@ -177,9 +180,9 @@ extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int3
     for (uint64_t i = 0; i < n_chunks; ++i) p->free_ids[i] = (uint32_t)(n_chunks - 1 - i);
     *out = p;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_pool_destroy(sllm_pool* p) {
+extern "C" int32_t sllm_pool_destroy(sllm_pool* p) try {
     clear_error();
     if (!p) return SLLM_OK;
     {
@@ -189,9 +192,9 @@ extern "C" int32_t sllm_pool_destroy(sllm_pool* p) {
     DeviceGuard guard(p->device);
     destroy_pool(p);
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_pool_query(const sllm_pool* pc, sllm_pool_info* out) {
+extern "C" int32_t sllm_pool_query(const sllm_pool* pc, sllm_pool_info* out) try {
     clear_error();
     if (!pc || !out) return fail(SLLM_E_INVAL, "pool and out must be non-NULL");
     auto* p = const_cast<sllm_pool*>(pc);
@@ -201,9 +204,9 @@ extern "C" int32_t sllm_pool_query(const sllm_pool* pc, sllm_pool_info* out) {
     out->free_chunks = p->free_ids.size();
     out->cached_checkpoints = p->cache.size();
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_threads, uint32_t flags) {
+extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_threads, uint32_t flags) try {
     clear_error();
     if (!p || !dir) return fail(SLLM_E_INVAL, "pool and dir must be non-NULL");
     if (flags & ~SLLM_OPEN_DIRECT_IO) return fail(SLLM_E_INVAL, "unknown flags 0x%x", flags);
@@ -276,9 +279,9 @@ extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_th
     }
     p->cache.push_back(std::move(e));
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_pool_evict(sllm_pool* p, const char* dir) {
+extern "C" int32_t sllm_pool_evict(sllm_pool* p, const char* dir) try {
     clear_error();
     if (!p || !dir) return fail(SLLM_E_INVAL, "pool and dir must be non-NULL");
     const std::string canon = canonical(dir);
@@ -299,4 +302,4 @@ extern "C" int32_t sllm_pool_evict(sllm_pool* p, const char* dir) {
         return SLLM_OK;
     }
     return fail(SLLM_E_NOTFOUND, "%s is not cached", dir);
-}
+} SLLM_CATCH_ALL

@@ -119,11 +119,17 @@ int32_t read_header(int fd, uint64_t file_size, const char* path, uint64_t* data
 }  // namespace
 
 extern "C" int32_t sllm_convert_safetensors(const char* const* paths, uint64_t n_paths, const char* out_dir,
-                                            const sllm_convert_opts* opts) {
+                                            const sllm_convert_opts* opts) try {
     clear_error();
     if ((n_paths && !paths) || !out_dir) return fail(SLLM_E_INVAL, "paths and out_dir must be non-NULL");
     sllm_writer* w = nullptr;
     SLLM_TRY(sllm_writer_open(out_dir, opts, &w));
+    struct Abort {  // removes the partial output unless the writer was closed
+        sllm_writer*& w;
+        ~Abort() {
+            if (w) sllm_writer_abort(w);
+        }
+    } abort_guard{w};
     std::vector<uint8_t> buf;
     int32_t st = SLLM_OK;
     std::string msg;
@@ -134,6 +140,10 @@ extern "C" int32_t sllm_convert_safetensors(const char* const* paths, uint64_t n
             st = fail(path ? SLLM_E_IO : SLLM_E_INVAL, "open %s: %s", path ? path : "(null)", path ? std::strerror(errno) : "");
             break;
         }
+        struct Closer {
+            int fd;
+            ~Closer() { ::close(fd); }
+        } closer{fd};
         struct stat sb;
         std::vector<Entry> entries;
         uint64_t data_start = 0;
@@ -149,12 +159,14 @@ extern "C" int32_t sllm_convert_safetensors(const char* const* paths, uint64_t n
                               nbytes ? buf.data() : nullptr, nbytes};
             st = sllm_writer_add(w, &t);
         }
-        ::close(fd);
     }
     if (st != SLLM_OK) {
         msg = sllm_last_error();
         sllm_writer_abort(w);
+        w = nullptr;
         return fail(st, "%s", msg.c_str());
     }
-    return sllm_writer_close(w);
-}
+    sllm_writer* done = w;
+    w = nullptr;
+    return sllm_writer_close(done);
+} SLLM_CATCH_ALL

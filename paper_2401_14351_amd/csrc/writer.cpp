@@ -113,7 +113,7 @@ int32_t write_file(const std::string& path, const std::string& bytes, bool do_fs
 
 }  // namespace
 
-extern "C" int32_t sllm_writer_open(const char* out_dir, const sllm_convert_opts* opts, sllm_writer** out) {
+extern "C" int32_t sllm_writer_open(const char* out_dir, const sllm_convert_opts* opts, sllm_writer** out) try {
     clear_error();
     if (!out_dir || !out) return fail(SLLM_E_INVAL, "out_dir and out must be non-NULL");
     *out = nullptr;
@@ -147,9 +147,9 @@ extern "C" int32_t sllm_writer_open(const char* out_dir, const sllm_convert_opts
     }
     *out = w;
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* t) {
+extern "C" int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* t) try {
     clear_error();
     if (!w || !t) return fail(SLLM_E_INVAL, "writer and tensor must be non-NULL");
     if (w->error != SLLM_OK) return fail(w->error, "writer already failed");
@@ -176,9 +176,9 @@ extern "C" int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* t) {
     r.nbytes = t->nbytes;
     w->recs.push_back(std::move(r));
     return SLLM_OK;
-}
+} SLLM_CATCH_ALL
 
-extern "C" int32_t sllm_writer_close(sllm_writer* w) {
+extern "C" int32_t sllm_writer_close(sllm_writer* w) try {
     clear_error();
     if (!w) return fail(SLLM_E_INVAL, "writer is NULL");
     int32_t st = w->error;
@@ -206,14 +206,14 @@ extern "C" int32_t sllm_writer_close(sllm_writer* w) {
     }
     destroy(w, st != SLLM_OK);
     return st;
-}
+} SLLM_CATCH_ALL
 
 extern "C" void sllm_writer_abort(sllm_writer* w) {
     if (w) destroy(w, true);
 }
 
 extern "C" int32_t sllm_convert(const sllm_src_tensor* tensors, uint64_t n, const char* out_dir,
-                                const sllm_convert_opts* opts) {
+                                const sllm_convert_opts* opts) try {
     clear_error();
     if (n && !tensors) return fail(SLLM_E_INVAL, "tensors is NULL");
     sllm_writer* w = nullptr;
@@ -227,4 +227,4 @@ extern "C" int32_t sllm_convert(const sllm_src_tensor* tensors, uint64_t n, cons
         }
     }
     return sllm_writer_close(w);
-}
+} SLLM_CATCH_ALL

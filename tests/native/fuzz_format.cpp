@@ -10,6 +10,7 @@
 //     exactly the same bytes.
 #include <cstdio>
 #include <cstdlib>
+#include <algorithm>
 #include <cstring>
 #include <fstream>
 #include <random>
@@ -18,6 +19,7 @@
 #include <vector>
 
 #include "format.hpp"
+#include "json.hpp"
 #include "sllm.h"
 
 using namespace sllm;
@@ -112,6 +114,36 @@ int main(int argc, char** argv) {
             CHECK(encode_index(ix) == m);
         }
     }
-    std::printf("ok rounds=60 mutants=%ld accepted=%ld\n", iters, accepted);
+    // 3. The safetensors header reader: mutations of a realistic header must
+    //    parse or fail cleanly, never read out of bounds.
+    const std::string header =
+        "{\"__metadata__\":{\"format\":\"pt\"},\"model.embed.weight\":{\"dtype\":\"BF16\","
+        "\"shape\":[32000,4096],\"data_offsets\":[0,262144000]},\"a\\u00e9\\ud83d\\ude00\":{\"dtype\":"
+        "\"F32\",\"shape\":[],\"data_offsets\":[262144000,262144004]},\"n\":[1.5e3,-0,true,false,null]}";
+    {
+        json::Value v;
+        json::Parser p(header.data(), header.size());
+        CHECK(p.parse(&v) && v.kind == json::Value::Object && v.fields.size() == 4);
+        CHECK(v.fields[2].first == "a\xc3\xa9\xf0\x9f\x98\x80");
+    }
+    long parsed = 0;
+    for (long it = 0; it < iters / 2; ++it) {
+        std::string m = header;
+        const int edits = 1 + (int)(rng() % 6);
+        for (int k = 0; k < edits; ++k) {
+            const int kind = (int)(rng() % 3);
+            const size_t at = rng() % (m.size() + 1);
+            if (kind == 0 && !m.empty()) m.erase(rng() % m.size(), 1 + rng() % 8);
+            else if (kind == 1) {
+                static const char alphabet[] = "{}[],:\"\\u0e-1 ";
+                m.insert(m.begin() + (long)std::min(at, m.size()), alphabet[rng() % (sizeof alphabet - 1)]);
+            }
+            else if (!m.empty()) m[rng() % m.size()] = (char)(rng() & 0xFF);
+        }
+        json::Value v;
+        json::Parser p(m.data(), m.size());
+        parsed += p.parse(&v);
+    }
+    std::printf("ok rounds=60 mutants=%ld accepted=%ld json_parsed=%ld\n", iters, accepted, parsed);
     return 0;
 }
