@@ -262,6 +262,10 @@ typedef struct sllm_stats {
     uint64_t bytes_bounced;     /* direct-read bytes staged through a bounce buffer
                                    because the kernel refused direct transfers
                                    into the pinned chunks                      */
+    double   reader_busy_s;     /* streamed loads: I/O-thread time spent reading
+                                   (summed over threads)                       */
+    double   reader_starved_s;  /* streamed loads: I/O-thread time spent waiting
+                                   for a free slot (summed over threads)       */
 } sllm_stats;
 int32_t sllm_get_stats(const sllm_ckpt* h, sllm_stats* out);
 

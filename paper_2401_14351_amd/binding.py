@@ -62,7 +62,7 @@ class Stats(C.Structure):
                 ("n_launches", C.c_uint64), ("engine", C.c_uint32), ("direct_io", C.c_uint32),
                 ("from_cache", C.c_uint32), ("io_threads", C.c_uint32), ("open_s", C.c_double),
                 ("load_s", C.c_double), ("read_wait_s", C.c_double), ("device_ms", C.c_double),
-                ("bytes_bounced", C.c_uint64)]
+                ("bytes_bounced", C.c_uint64), ("reader_busy_s", C.c_double), ("reader_starved_s", C.c_double)]
 
 
 class IpcDesc(C.Structure):

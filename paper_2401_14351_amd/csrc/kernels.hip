@@ -107,11 +107,13 @@ __global__ __launch_bounds__(kThreads) void k1_gather_bytes(GatherArgs a, uint64
     }
 }
 
+// A non-negative integer from the environment, or dflt when unset or malformed.
 uint32_t env_u32(const char* name, uint32_t dflt) {
     const char* s = std::getenv(name);
     if (!s || !*s) return dflt;
-    long v = std::strtol(s, nullptr, 10);
-    return v > 0 ? (uint32_t)v : dflt;
+    char* end = nullptr;
+    const long v = std::strtol(s, &end, 10);
+    return (end && *end == '\0' && v >= 0) ? (uint32_t)v : dflt;
 }
 
 }  // namespace
@@ -120,6 +122,7 @@ GatherShape gather_shape() {
     // read at every launch (a few getenv calls) so one process can compare shapes
     GatherShape s;
     s.blocks = env_u32("SLLM_K1_BLOCKS", 512);
+    if (s.blocks == 0) s.blocks = 1;
     s.unroll = env_u32("SLLM_K1_UNROLL", 4);
     if (s.unroll != 1 && s.unroll != 2 && s.unroll != 4) s.unroll = 4;
     s.nontemporal = env_u32("SLLM_K1_NT", 0) != 0;

@@ -277,10 +277,13 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
     }
 }
 
-uint32_t env_blocks(const char* name, uint32_t dflt) {
+// A non-negative integer from the environment, or dflt when unset or malformed.
+uint32_t env_uint(const char* name, uint32_t dflt) {
     const char* s = std::getenv(name);
-    long v = s ? std::strtol(s, nullptr, 10) : 0;
-    return v > 0 ? (uint32_t)v : dflt;
+    if (!s || !*s) return dflt;
+    char* end = nullptr;
+    const long v = std::strtol(s, &end, 10);
+    return (end && *end == '\0' && v >= 0) ? (uint32_t)v : dflt;
 }
 
 // first device byte owned by partition byte x: the first tensor whose data
@@ -303,13 +306,13 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     a.total = l.total;
     if (a.y0 >= a.y1 || l.n == 0) return SLLM_OK;
     if (a.y1 > l.dev_total) return fail(SLLM_E_INVAL, "scatter: destination range past the image");
-    const uint32_t unroll = env_blocks("SLLM_K2_UNROLL", 8) >= 8 ? 8 : 4;
-    const bool nt = env_blocks("SLLM_K2_NT", 0) == 1 && !src_is_host;
+    const uint32_t unroll = env_uint("SLLM_K2_UNROLL", 8) >= 8 ? 8 : 4;
+    const bool nt = env_uint("SLLM_K2_NT", 1) != 0 && !src_is_host;
     const uint64_t tile = (uint64_t)kThreads * 16 * unroll;
     a.tile0 = a.y0 / tile;
     a.n_tiles = ceil_div(a.y1, tile) - a.tile0;
     // host sources are PCIe-latency bound like K1; HBM sources want a full chip
-    const uint32_t want = src_is_host ? env_blocks("SLLM_K1_BLOCKS", 512) : env_blocks("SLLM_K2_BLOCKS", 1024);
+    const uint32_t want = std::max<uint32_t>(1, src_is_host ? env_uint("SLLM_K1_BLOCKS", 512) : env_uint("SLLM_K2_BLOCKS", 2048));
     const dim3 grid((uint32_t)std::min<uint64_t>(a.n_tiles, want)), block(kThreads);
     if (unroll == 8) {
         if (nt) k_scatter<8, true><<<grid, block, 0, stream>>>(a);

@@ -11,6 +11,7 @@
 //    refilled only after its event has fired.
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <condition_variable>
 #include <cstring>
 #include <deque>
@@ -31,8 +32,13 @@ struct Slot {
     uint32_t id = 0;                  // pool chunk id
     uint8_t* host = nullptr;
     const uint8_t* mapped = nullptr;  // device-visible address of the same bytes
-    hipEvent_t done = nullptr;        // fires when the GPU no longer reads the slot
-    bool pending = false;
+    hipEvent_t done = nullptr;        // the event of a batch this slot heads
+};
+
+// A batch of slots the GPU may still read, and the event that ends it.
+struct InFlight {
+    hipEvent_t ev = nullptr;
+    std::vector<uint32_t> slots;
 };
 
 }  // namespace
@@ -53,6 +59,7 @@ struct sllm_ckpt {
     uint32_t io_threads = 4, n_streams = 2, ring_slots = 8, engine = SLLM_ENGINE_KERNEL, flags = 0;
     std::vector<Slot> slots;
     std::vector<uint32_t> slot_ids;
+    std::deque<InFlight> inflight;  // batches of the last streamed load not yet seen done
     std::vector<hipStream_t> streams;
     std::vector<hipEvent_t> join_ev;
     hipEvent_t fork_ev = nullptr, t0_ev = nullptr, t1_ev = nullptr;
@@ -70,11 +77,9 @@ void release(sllm_ckpt* h) {
     if (used_hip) {
         DeviceGuard guard(h->device);
         for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
+        for (const InFlight& b : h->inflight) (void)hipEventSynchronize(b.ev);
         for (Slot& s : h->slots)
-            if (s.done) {
-                if (s.pending) (void)hipEventSynchronize(s.done);
-                (void)hipEventDestroy(s.done);
-            }
+            if (s.done) (void)hipEventDestroy(s.done);
         for (hipEvent_t e : h->join_ev) (void)hipEventDestroy(e);
         for (hipEvent_t e : {h->fork_ev, h->t0_ev, h->t1_ev})
             if (e) (void)hipEventDestroy(e);
@@ -190,12 +195,26 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     return join_streams(h, user);
 }
 
-// The streamed pipeline: io_threads readers feed the issue loop through two queues.
+// The streamed pipeline: io_threads readers feed the issue loop through two
+// queues.  Readers only read: they take a free slot, fill it with the next
+// chunk and queue it.  The issue loop owns every device call: it moves each
+// pass's ready chunks (one batched gather, or one copy / scatter), records
+// one event per batch, and returns a batch's slots to the free queue once
+// that event has completed, polling in-flight batches in order and blocking
+// on the oldest only when every slot is on the GPU.  Batches still in flight
+// when the load returns are reclaimed at the start of the next one.
+int32_t reclaim_all(sllm_ckpt* h) {
+    for (const InFlight& b : h->inflight) SLLM_HIP(hipEventSynchronize(b.ev));
+    h->inflight.clear();
+    return SLLM_OK;
+}
+
 int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     const uint64_t C = h->chunk, T = h->ix.total;
     const uint64_t n = ceil_div(T, C);
     const uint64_t read_end = h->file.direct ? h->ix.file_bytes : T;
     h->stats.n_chunks = n;
+    SLLM_TRY(reclaim_all(h));
     SLLM_TRY(fork_streams(h, user));
 
     std::mutex mu;
@@ -204,10 +223,12 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     std::deque<std::pair<uint64_t, uint32_t>> ready_q;
     for (uint32_t i = 0; i < h->slots.size(); ++i) free_q.push_back(i);
     std::atomic<uint64_t> next{0};
+    uint32_t reading = 0;  // slots held by readers
     bool stop = false;
     int32_t err = SLLM_OK;
     std::string err_msg;
     uint64_t bytes_read = 0, bytes_bounced = 0;
+    std::atomic<uint64_t> busy_ns{0}, starved_ns{0};
 
     auto set_error = [&](int32_t st) {  // caller holds mu
         if (err == SLLM_OK) {
@@ -220,29 +241,27 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     };
 
     auto reader = [&] {
-        (void)hipSetDevice(h->device);
         for (;;) {
             const uint64_t k = next.fetch_add(1);
             if (k >= n) return;
             uint32_t si;
             {
+                const double w0 = now_s();
                 std::unique_lock<std::mutex> lk(mu);
                 cv_free.wait(lk, [&] { return stop || !free_q.empty(); });
+                starved_ns += (uint64_t)((now_s() - w0) * 1e9);
                 if (stop) return;
                 si = free_q.front();
                 free_q.pop_front();
-            }
-            Slot& s = h->slots[si];
-            int32_t st = SLLM_OK;
-            if (s.pending) {
-                hipError_t e = hipEventSynchronize(s.done);
-                if (e != hipSuccess) st = fail(SLLM_E_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
-                s.pending = false;
+                ++reading;
             }
             const uint64_t off = k * C, len = std::min(C, read_end - off);
             uint64_t bounced = 0;
-            if (st == SLLM_OK) st = read_chunk(h->file, s.host, len, off, h->data_path, &bounced);
+            const double r0 = now_s();
+            const int32_t st = read_chunk(h->file, h->slots[si].host, len, off, h->data_path, &bounced);
+            busy_ns += (uint64_t)((now_s() - r0) * 1e9);
             std::lock_guard<std::mutex> g(mu);
+            --reading;
             if (st != SLLM_OK) {
                 free_q.push_back(si);
                 set_error(st);
@@ -271,6 +290,24 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         return fail(SLLM_E_NOMEM, "cannot start %u I/O threads", nt);
     }
 
+    // give the slots of completed batches back to the readers; with `block`,
+    // wait for the oldest batch first
+    auto reclaim = [&](bool block) -> int32_t {
+        while (!h->inflight.empty()) {
+            hipError_t e = block ? hipEventSynchronize(h->inflight.front().ev) : hipEventQuery(h->inflight.front().ev);
+            block = false;
+            if (e == hipErrorNotReady) break;
+            if (e != hipSuccess) return fail(SLLM_E_HIP, "waiting for a batch: %s", hipGetErrorString(e));
+            {
+                std::lock_guard<std::mutex> g(mu);
+                for (uint32_t si : h->inflight.front().slots) free_q.push_back(si);
+            }
+            cv_free.notify_all();
+            h->inflight.pop_front();
+        }
+        return SLLM_OK;
+    };
+
     // kernel loads in the file layout move every chunk that is ready in one
     // batched gather; the other paths move one chunk per call
     const uint32_t max_batch = (h->engine == SLLM_ENGINE_KERNEL && !h->dev_align) ? kGatherBatch : 1;
@@ -278,22 +315,35 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     batch.reserve(max_batch);
     double wait_s = 0;
     uint64_t moved = 0, launches = 0;
-    while (moved < n) {
+    int32_t rc = SLLM_OK;
+    while (moved < n && rc == SLLM_OK) {
+        rc = reclaim(false);
+        if (rc != SLLM_OK) break;
         batch.clear();
+        bool wait_gpu = false;
         {
             const double w0 = now_s();
             std::unique_lock<std::mutex> lk(mu);
-            cv_ready.wait(lk, [&] { return stop || !ready_q.empty(); });
+            if (ready_q.empty() && !stop) {
+                if (free_q.empty() && reading == 0 && !h->inflight.empty())
+                    wait_gpu = true;  // every slot is on the GPU
+                else
+                    cv_ready.wait_for(lk, std::chrono::microseconds(200), [&] { return stop || !ready_q.empty(); });
+            }
             wait_s += now_s() - w0;
-            if (ready_q.empty()) break;  // stopped by a reader's error
+            if (stop && ready_q.empty()) break;  // a reader failed
             while (!ready_q.empty() && batch.size() < max_batch) {
                 batch.push_back(ready_q.front());
                 ready_q.pop_front();
             }
         }
+        if (wait_gpu) {
+            rc = reclaim(true);
+            continue;
+        }
+        if (batch.empty()) continue;
         const uint32_t si = (uint32_t)(launches % h->streams.size());
         hipStream_t st = h->streams[si];
-        int32_t rc;
         if (max_batch > 1) {
             const uint8_t* srcs[kGatherBatch];
             uint64_t ks[kGatherBatch];
@@ -307,26 +357,28 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             const Slot& s0 = h->slots[batch[0].second];
             rc = move_chunk(h, dst, k, s0.host, s0.mapped, std::min(C, T - k * C), si, st);
         }
-        for (size_t b = 0; rc == SLLM_OK && b < batch.size(); ++b) {
-            hipError_t e = hipEventRecord(h->slots[batch[b].second].done, st);
+        InFlight f;
+        f.ev = h->slots[batch[0].second].done;  // free: its slot is not in another batch
+        if (rc == SLLM_OK) {
+            hipError_t e = hipEventRecord(f.ev, st);
             if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
         }
+        for (const auto& item : batch) f.slots.push_back(item.second);
+        if (rc == SLLM_OK) {
+            h->inflight.push_back(std::move(f));
+        } else {  // nothing of this batch reached the GPU: its slots are free
+            std::lock_guard<std::mutex> g(mu);
+            for (uint32_t s2 : f.slots) free_q.push_back(s2);
+        }
         ++launches;
-        std::lock_guard<std::mutex> g(mu);
-        for (const auto& item : batch) {
-            if (rc == SLLM_OK) h->slots[item.second].pending = true;
-            free_q.push_back(item.second);
-        }
-        if (rc != SLLM_OK) {
-            set_error(rc);
-            break;
-        }
         moved += batch.size();
-        cv_free.notify_all();
     }
     {
+        // after a complete pass every chunk has been read, so no reader waits
+        // for a slot; after an error, stop releases the ones that do
         std::lock_guard<std::mutex> g(mu);
-        if (err != SLLM_OK) stop = true;
+        if (rc != SLLM_OK) set_error(rc);
+        stop = true;
         cv_free.notify_all();
     }
     for (auto& t : threads) t.join();
@@ -334,8 +386,11 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     h->stats.bytes_read = bytes_read;
     h->stats.bytes_bounced = bytes_bounced;
     h->stats.n_launches = launches;
+    h->stats.reader_busy_s = (double)busy_ns.load() * 1e-9;
+    h->stats.reader_starved_s = (double)starved_ns.load() * 1e-9;
     if (err != SLLM_OK) {
         for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);  // drain in-flight copies
+        h->inflight.clear();
         return fail(err, "%s", err_msg.c_str());
     }
     return join_streams(h, user);
@@ -524,6 +579,8 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
     h->stats.from_cache = 0;
     h->stats.read_wait_s = 0;
     h->stats.bytes_bounced = 0;
+    h->stats.reader_busy_s = 0;
+    h->stats.reader_starved_s = 0;
     h->stats.device_ms = -1;
     h->timed = false;
     const bool timing = (h->flags & SLLM_OPEN_TIMING) != 0;
