@@ -489,6 +489,8 @@ def main():
                           "bytes_read": int(last_stats.get("bytes_read", 0)),
                           "bytes_bounced": int(last_stats.get("bytes_bounced", 0)),
                           "read_wait_s": round(last_stats.get("read_wait_s", 0.0), 4),
+                          "reader_busy_s": round(last_stats.get("reader_busy_s", 0.0), 3),
+                          "reader_starved_s": round(last_stats.get("reader_starved_s", 0.0), 3),
                           "device": block_device(d)}
 
     kernel_ms = [a.elapsed_time(b) for a, b in zip(ev0, ev1)]
