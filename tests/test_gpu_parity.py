@@ -429,28 +429,24 @@ def test_fragmented_pool(torch_cuda, opt125m, tmp_path):
     spec, tensors, d = opt125m
     want, _ = expected(tensors, spec.alignment)
     want2, _ = expected(tensors, spec.alignment, 256)
-    C = 4 << 20  # 60 chunks per copy of the checkpoint
-    small = synth.tiny(3, alignment=256)
-    small_t = tensors_of(small)
-    ds = str(tmp_path / "small")
-    binding.convert(iter(small_t), ds, 256, C)
-    other = str(tmp_path / "opt_copy")
-    binding.convert(iter(tensors), other, spec.alignment, C)
-    with binding.Pool(C, 130) as pool:
-        pool.cache(d)          # chunks 0..59
-        pool.cache(ds)         # chunk 60
-        pool.cache(other)      # chunks 61..120
-        pool.evict(d)
-        pool.evict(other)
-        pool.cache(other)      # takes the lowest free ids again
-        pool.evict(ds)
-        pool.cache(d)          # now spread over the holes
-        info = pool.info()
-        assert info["cached_checkpoints"] == 2
+    C = 4 << 20  # the OPT-125M partition takes 60 chunks
+    smalls = []
+    for i in range(24):  # one-chunk checkpoints
+        sp = synth.tiny(100 + i, alignment=256)
+        sd = str(tmp_path / f"s{i}")
+        binding.convert(iter(tensors_of(sp)), sd, 256, C)
+        smalls.append(sd)
+    with binding.Pool(C, 24 + 60) as pool:
+        for sd in smalls:
+            pool.cache(sd)          # chunks 0..23
+        for sd in smalls[::2]:
+            pool.evict(sd)          # holes at 0, 2, ..., 22
+        pool.cache(d)               # 12 holes, then chunks 24..71
         for engine in ("kernel", "sdma"):
             for a2, ref in ((0, want), (256, want2)):
                 with binding.Checkpoint(d, pool=pool, engine=engine, dev_alignment=a2) as ck:
                     assert_same(run_load(torch, ck, len(ref)), ref, f"fragmented {engine} A2={a2}")
         pool.evict(d)
-        pool.evict(other)
-        assert pool.info()["free_chunks"] == 130
+        for sd in smalls[1::2]:
+            pool.evict(sd)
+        assert pool.info()["free_chunks"] == 24 + 60
