@@ -101,7 +101,9 @@ int32_t read_error(int e, const std::string& path, uint64_t off) {
     return fail(SLLM_E_IO, "read %s at %llu: %s", path.c_str(), (unsigned long long)off, std::strerror(e));
 }
 
-constexpr uint64_t kBounceBytes = 4u << 20;
+// 16 MiB: one read of a 16 MiB chunk, which the block layer splits into
+// several requests in flight at once (a deeper queue than 4 MiB reads give)
+constexpr uint64_t kBounceBytes = 16u << 20;
 
 struct Bounce {
     void* p = nullptr;

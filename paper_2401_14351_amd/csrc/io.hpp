@@ -33,7 +33,7 @@ int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const
 // Read one chunk into a pinned pool chunk.  With O_DIRECT the bytes go
 // straight into `dst`; where the kernel refuses direct transfers into that
 // memory (EFAULT: the pages cannot be pinned for I/O), they go through a
-// 4 MiB aligned per-thread bounce buffer instead, and *bounced counts them.
+// 16 MiB aligned per-thread bounce buffer instead, and *bounced counts them.
 int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
                    uint64_t* bounced);
 

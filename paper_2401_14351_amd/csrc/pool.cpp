@@ -126,6 +126,31 @@ void destroy_pool(sllm_pool* p) {
     delete p;
 }
 
+// Touch every 4 KiB page of the new arenas once, from several threads, so
+// that the CPU page tables of the pinned memory are populated when the pool
+// is created: the first CPU write to a page of a fresh pinned allocation
+// takes a page fault, which would otherwise be paid by the first fill of
+// each chunk (the pool is a pre-allocated tier, Sec. 4.2).
+void prefault(const std::vector<void*>& arenas, uint64_t arena_bytes_last, uint64_t arena_bytes) {
+    constexpr uint64_t kPiece = 64ull << 20;
+    struct Piece {
+        uint8_t* p;
+        uint64_t n;
+    };
+    std::vector<Piece> pieces;
+    for (size_t a = 0; a < arenas.size(); ++a) {
+        const uint64_t n = a + 1 == arenas.size() ? arena_bytes_last : arena_bytes;
+        for (uint64_t o = 0; o < n; o += kPiece)
+            pieces.push_back({static_cast<uint8_t*>(arenas[a]) + o, std::min(kPiece, n - o)});
+    }
+    const unsigned hw = std::thread::hardware_concurrency();
+    (void)parallel_chunks(pieces.size(), std::min(16u, hw ? hw : 1u), -1, [&](uint64_t k) {
+        volatile uint8_t* p = pieces[k].p;
+        for (uint64_t o = 0; o < pieces[k].n; o += 4096) p[o] = 0;
+        return SLLM_OK;
+    });
+}
+
 std::string canonical(const char* dir) {
     char buf[PATH_MAX];
     return ::realpath(dir, buf) ? std::string(buf) : std::string(dir);
@@ -176,6 +201,11 @@ extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int3
         }
         done += k;
     }
+    const double t0 = now_s();
+    const uint64_t last = n_chunks - (p->arenas.size() - 1) * per_arena;
+    prefault(p->arenas, last * stride, per_arena * stride);
+    log_msg(2, "pool: %llu x %llu B pinned in %zu arenas, pages touched in %.3f s", (unsigned long long)n_chunks,
+            (unsigned long long)stride, p->arenas.size(), now_s() - t0);
     p->free_ids.resize(n_chunks);
     for (uint64_t i = 0; i < n_chunks; ++i) p->free_ids[i] = (uint32_t)(n_chunks - 1 - i);
     *out = p;

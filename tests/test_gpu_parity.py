@@ -450,3 +450,21 @@ def test_fragmented_pool(torch_cuda, opt125m, tmp_path):
         for sd in smalls[1::2]:
             pool.evict(sd)
         assert pool.info()["free_chunks"] == 24 + 60
+
+
+@pytest.mark.parametrize("A2", [16, 256, 4096])
+def test_offsets_scan_20000_tensors(torch_cuda, tmp_path, A2):
+    """20,000 tensors (the stress workload's count, here with small sizes):
+    the device offsets scan runs over 20 blocks of 1,024 entries with a
+    carry; sllm_open checks it against the host plan, and the loaded device
+    layout matches the oracle's."""
+    torch = torch_cuda
+    spec = synth.stress(n=20000, min_bytes=1, max_bytes=600, seed=77)
+    tensors = tensors_of(spec)
+    d = str(tmp_path)
+    binding.convert(iter(tensors), d, spec.alignment, 1 << 20)
+    want, index = expected(tensors, spec.alignment, A2)
+    d2, T2 = oracle.device_layout(index, A2)
+    with binding.Checkpoint(d, dev_alignment=A2, chunk_size=1 << 20) as ck:
+        assert [t.offset for t in ck.tensors()] == d2 and ck.total_bytes == T2
+        assert_same(run_load(torch, ck, len(want)), want, f"A2={A2}")
