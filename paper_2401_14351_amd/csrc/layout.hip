@@ -5,9 +5,10 @@
 //     wave, the 16 wave totals combined through LDS, a running carry across
 //     blocks of 1024 tensors.
 // K2  index-driven scatter (HBM source) and K1-scatter (mapped pinned host
-//     source): destination-driven.  Each workgroup owns a 16 or 32 KiB tile
-//     of the device image, finds the tensors whose slots meet the tile (binary
-//     search of d), stages those index entries in LDS, and then every lane
+//     source): destination-driven.  Each workgroup walks a contiguous span of
+//     16 or 32 KiB tiles of the device image, finds the tensors whose slots
+//     meet a tile (a forward search of d), stages those index entries in LDS
+//     and keeps them for the following tiles they still cover; every lane
 //     produces aligned 16-byte destination vectors: a straight 16-byte load
 //     when source and destination agree mod 16, two aligned loads and a byte
 //     funnel shift when they do not, zeros for padding.  Only vectors cut by
@@ -185,38 +186,51 @@ __device__ __forceinline__ void st16(uint8_t* p, u32x4 v) {
 }
 
 // One tile: every lane first produces its U destination vectors (all source
-// loads in flight together), then stores them.
+// loads in flight together), then stores them.  The index entries of the
+// tensors meeting a tile are staged in LDS together with the start of the
+// next tensor's slot; while the following tiles end before that start (the
+// interior of a large tensor) they reuse the staged entries, with no search,
+// no staging and no barrier.
 template <uint32_t U, bool NT>
 __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
     constexpr uint64_t kTileU = (uint64_t)kThreads * 16 * U;
     __shared__ uint64_t s_dev[kLdsEntries], s_off[kLdsEntries], s_size[kLdsEntries];
-    __shared__ uint64_t s_lo, s_hi;
+    __shared__ uint64_t s_lo, s_hi, s_next;
     const Src src{a};
     // each workgroup walks a contiguous span of tiles, so the owning tensor
     // of the next tile is found by searching forward from the last one
     const uint64_t per_block = (a.n_tiles + gridDim.x - 1) / gridDim.x;
     const uint64_t t_begin = (uint64_t)blockIdx.x * per_block;
     const uint64_t t_end = t_begin + per_block < a.n_tiles ? t_begin + per_block : a.n_tiles;
-    uint64_t cursor = 0;  // thread 0: owner of the previous tile's last byte
+    uint64_t cursor = 0;   // thread 0: owner of the last searched tile's last byte
+    bool staged = false;   // LDS holds entries i_lo .. i_lo + cnt - 1 (uniform)
+    uint64_t i_lo = 0, cnt = 0, next = 0;  // next: d of the first tensor not staged
     for (uint64_t t = t_begin; t < t_end; ++t) {
         const uint64_t yt = (a.tile0 + t) * kTileU;
         const uint64_t lo = yt > a.y0 ? yt : a.y0;
         const uint64_t hi = yt + kTileU < a.y1 ? yt + kTileU : a.y1;
-        if (threadIdx.x == 0) {
-            const uint64_t i_lo = t == t_begin ? owner_global(a.dev, 0, a.n - 1, lo) : owner_from(a.dev, cursor, a.n - 1, lo);
-            cursor = owner_from(a.dev, i_lo, a.n - 1, hi - 1);
-            s_lo = i_lo;
-            s_hi = cursor;
+        if (!staged || hi > next) {
+            __syncthreads();  // every wave is done with the entries staged before
+            if (threadIdx.x == 0) {
+                const uint64_t first =
+                    t == t_begin ? owner_global(a.dev, 0, a.n - 1, lo) : owner_from(a.dev, cursor, a.n - 1, lo);
+                cursor = owner_from(a.dev, first, a.n - 1, hi - 1);
+                s_lo = first;
+                s_hi = cursor;
+            }
+            __syncthreads();
+            i_lo = s_lo;
+            cnt = s_hi - s_lo + 1;
+            staged = cnt <= kLdsEntries;
+            if (staged && threadIdx.x < cnt) {
+                s_dev[threadIdx.x] = a.dev[i_lo + threadIdx.x];
+                s_off[threadIdx.x] = a.off[i_lo + threadIdx.x];
+                s_size[threadIdx.x] = a.size[i_lo + threadIdx.x];
+            }
+            if (threadIdx.x == 0) s_next = a.dev[i_lo + cnt];  // d[n] = T2 ends the last slot
+            __syncthreads();
+            next = s_next;
         }
-        __syncthreads();
-        const uint64_t i_lo = s_lo, cnt = s_hi - s_lo + 1;
-        const bool staged = cnt <= kLdsEntries;
-        if (staged && threadIdx.x < cnt) {
-            s_dev[threadIdx.x] = a.dev[i_lo + threadIdx.x];
-            s_off[threadIdx.x] = a.off[i_lo + threadIdx.x];
-            s_size[threadIdx.x] = a.size[i_lo + threadIdx.x];
-        }
-        __syncthreads();
         u32x4 v[U];
         uint32_t whole_mask = 0, in_mask = 0;
 #pragma unroll
@@ -273,7 +287,6 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
                     if (y + b >= lo && y + b < hi) a.dst[y + b] = (uint8_t)byte_of(v[u], b);
             }
         }
-        __syncthreads();  // LDS entries are restaged for the next tile
     }
 }
 
@@ -312,7 +325,7 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     a.tile0 = a.y0 / tile;
     a.n_tiles = ceil_div(a.y1, tile) - a.tile0;
     // host sources are PCIe-latency bound like K1; HBM sources want a full chip
-    const uint32_t want = std::max<uint32_t>(1, src_is_host ? env_uint("SLLM_K1_BLOCKS", 512) : env_uint("SLLM_K2_BLOCKS", 2048));
+    const uint32_t want = std::max<uint32_t>(1, src_is_host ? env_uint("SLLM_K1_BLOCKS", 512) : env_uint("SLLM_K2_BLOCKS", 8192));
     const dim3 grid((uint32_t)std::min<uint64_t>(a.n_tiles, want)), block(kThreads);
     if (unroll == 8) {
         if (nt) k_scatter<8, true><<<grid, block, 0, stream>>>(a);
