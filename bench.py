@@ -43,10 +43,19 @@ REGIME = {"dram": "warm host DRAM (pinned pool)",
           "direct": "file through pinned ring slots (O_DIRECT reads)"}
 
 
-def profiled_counters(summary: str, source: str):
+def kernel_source_hash(*sources: str) -> str:
+    """SHA-256 over the kernel's source files (csrc/), in the order given."""
+    h = hashlib.sha256()
+    for name in sources:
+        h.update(open(os.path.join(ROOT, "paper_2401_14351_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
+def profiled_counters(summary: str, *sources: str):
     """Counter figures recorded in profiles/<summary> ('counters: {json}' line),
-    or None when that file is missing or the kernel source has changed since
-    the counters were taken (its SHA-256 no longer matches)."""
+    or None when that file is missing or the kernel's sources (the .hip file
+    and the header that shapes its arguments) have changed since the counters
+    were taken (their SHA-256 no longer matches)."""
     path = os.path.join(ROOT, "profiles", summary)
     if not os.path.exists(path):
         return None
@@ -56,8 +65,11 @@ def profiled_counters(summary: str, source: str):
             rec = json.loads(line[len("counters: "):])
     if rec is None:
         return None
-    src = open(os.path.join(ROOT, "paper_2401_14351_amd", "csrc", source), "rb").read()
-    return rec if hashlib.sha256(src).hexdigest() == rec.get("source_sha256") else None
+    return rec if kernel_source_hash(*sources) == rec.get("source_sha256") else None
+
+
+K1_SOURCES = ("kernels.hip", "kernels.hpp")
+K2_SOURCES = ("layout.hip", "device_layout.hpp")
 
 
 def log(*a):
@@ -380,7 +392,7 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
             if i:
                 ms.append(e0.elapsed_time(e1))
         k2 = (T + T2) / (statistics.mean(ms) * 1e-3) / 1e9
-        k2c = profiled_counters("k_scatter_repack_llama-2-7b.md", "layout.hip")
+        k2c = profiled_counters("k_scatter_repack_llama-2-7b.md", *K2_SOURCES)
         out["repack_k2"] = {"dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
                             "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1),
                             "bound": "hbm", "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),
@@ -543,6 +555,8 @@ def main():
                           "direct_io": int(last_stats.get("direct_io", 0)),
                           "bytes_read": int(last_stats.get("bytes_read", 0)),
                           "bytes_bounced": int(last_stats.get("bytes_bounced", 0)),
+                          "chunks": int(last_stats.get("n_chunks", 0)),
+                          "launches": int(last_stats.get("n_launches", 0)),
                           "read_wait_s": round(last_stats.get("read_wait_s", 0.0), 4),
                           "reader_busy_s": round(last_stats.get("reader_busy_s", 0.0), 3),
                           "reader_starved_s": round(last_stats.get("reader_starved_s", 0.0), 3),
@@ -552,7 +566,7 @@ def main():
     k_avg_s = statistics.mean(kernel_ms) * 1e-3
     achieved = T / k_avg_s / 1e9
     value = T * args.steps / elapsed / 1e9
-    k1_counters = (profiled_counters("k1_gather_llama-2-7b.md", "kernels.hip")
+    k1_counters = (profiled_counters("k1_gather_llama-2-7b.md", *K1_SOURCES)
                    if cached and args.engine == "kernel" and spec.name == "llama-2-7b" and C == 16 << 20
                    and not args.dev_alignment else None)
     out = {

@@ -25,7 +25,7 @@ struct GatherLaunch {
 int32_t launch_gather(const GatherLaunch& g, hipStream_t stream);
 
 // Up to this many chunks, each from its own slot, in one gather launch.
-constexpr uint32_t kGatherBatch = 16;
+constexpr uint32_t kGatherBatch = 64;
 
 // Gather n (<= kGatherBatch) chunks: chunk chunks[i] of the partition from
 // the device-visible slot srcs[i] into dst + chunks[i] * C.

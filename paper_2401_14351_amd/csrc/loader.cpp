@@ -203,6 +203,8 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
 // that event has completed, polling in-flight batches in order and blocking
 // on the oldest only when every slot is on the GPU.  Batches still in flight
 // when the load returns are reclaimed at the start of the next one.
+constexpr uint64_t kBatchTargetBytes = 16ull << 20;
+
 int32_t reclaim_all(sllm_ckpt* h) {
     for (const InFlight& b : h->inflight) SLLM_HIP(hipEventSynchronize(b.ev));
     h->inflight.clear();
@@ -309,8 +311,17 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     };
 
     // kernel loads in the file layout move every chunk that is ready in one
-    // batched gather; the other paths move one chunk per call
-    const uint32_t max_batch = (h->engine == SLLM_ENGINE_KERNEL && !h->dev_align) ? kGatherBatch : 1;
+    // batched gather; the other paths move one chunk per call.  A batch's
+    // slots come back together, so a batch holds at most a quarter of the
+    // ring: four batches can be on the GPU while readers refill the rest.
+    const uint32_t max_batch =
+        (h->engine == SLLM_ENGINE_KERNEL && !h->dev_align)
+            ? std::max<uint32_t>(1, std::min<uint32_t>(kGatherBatch, (uint32_t)h->slots.size() / 4))
+            : 1;
+    // a short batch is held back while the GPU still has two batches queued
+    // and readers are filling slots, so that launches carry about
+    // kBatchTargetBytes each instead of whatever chunks arrived last
+    const uint64_t target = std::min<uint64_t>(max_batch, std::max<uint64_t>(1, kBatchTargetBytes / C));
     std::vector<std::pair<uint64_t, uint32_t>> batch;
     batch.reserve(max_batch);
     double wait_s = 0;
@@ -330,6 +341,11 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
                 else
                     cv_ready.wait_for(lk, std::chrono::microseconds(200), [&] { return stop || !ready_q.empty(); });
             }
+            const uint64_t fill = std::min<uint64_t>(target, n - moved);
+            if (!wait_gpu && !stop && ready_q.size() < fill && h->inflight.size() >= 2 &&
+                (reading > 0 || !free_q.empty()))
+                cv_ready.wait_for(lk, std::chrono::microseconds(100),
+                                  [&] { return stop || ready_q.size() >= fill; });
             wait_s += now_s() - w0;
             if (stop && ready_q.empty()) break;  // a reader failed
             while (!ready_q.empty() && batch.size() < max_batch) {

@@ -368,7 +368,8 @@ def test_gather_shapes(torch_cuda, opt125m, shape, monkeypatch):
 @pytest.mark.parametrize("C", [64 << 10, (64 << 10) + 48, 1 << 20])
 def test_streamed_batches(torch_cuda, opt125m, engine, C):
     """Many small chunks through a deep ring: the issue loop moves every
-    ready chunk of a pass in one batched gather (up to 16 slots)."""
+    ready chunk of a pass in one batched gather (up to 64 slots, at most a
+    quarter of the ring)."""
     torch = torch_cuda
     spec, tensors, d = opt125m
     want, _ = expected(tensors, spec.alignment)
