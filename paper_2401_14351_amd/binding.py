@@ -11,9 +11,12 @@ there is no fallback.
 from __future__ import annotations
 
 import ctypes as C
+import functools
 import os
-from dataclasses import dataclass
-from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+import threading
+from typing import Callable, Dict, Iterable, List, NamedTuple, Optional, Sequence, Tuple
+
+import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libsllm.so")
@@ -55,6 +58,12 @@ class OpenOpts(C.Structure):
 class TensorInfo(C.Structure):
     _fields_ = [("name", C.c_char_p), ("dtype", C.c_uint32), ("ndim", C.c_uint32),
                 ("shape", C.c_int64 * MAX_NDIM), ("offset", C.c_uint64), ("nbytes", C.c_uint64)]
+
+
+# the same layout as TensorInfo, for decoding a whole table with numpy
+_TENSOR_INFO = np.dtype([("name", "<u8"), ("dtype", "<u4"), ("ndim", "<u4"), ("shape", "<i8", (MAX_NDIM,)),
+                         ("offset", "<u8"), ("nbytes", "<u8")], align=True)
+assert _TENSOR_INFO.itemsize == C.sizeof(TensorInfo)
 
 
 class Stats(C.Structure):
@@ -279,8 +288,10 @@ class Pool:
         self.close()
 
 
-@dataclass(frozen=True)
-class Tensor:
+class Tensor(NamedTuple):
+    """One entry of the tensor index: offset is o_i (or d_i with a device
+    layout), nbytes the unpadded size."""
+
     name: str
     dtype: str
     shape: Tuple[int, ...]
@@ -310,10 +321,18 @@ class Checkpoint:
     def tensors(self) -> List[Tensor]:
         n = C.c_uint64()
         check(lib().sllm_tensor_index(self._h, None, 0, C.byref(n)))
-        arr = (TensorInfo * max(1, n.value))()
+        if n.value == 0:
+            return []
+        arr = (TensorInfo * n.value)()
         check(lib().sllm_tensor_index(self._h, arr, n.value, C.byref(n)))
-        return [Tensor(t.name.decode(), CODE_DTYPE[t.dtype], tuple(t.shape[:t.ndim]), t.offset, t.nbytes)
-                for t in arr[:n.value]]
+        # decode the whole table at once (per-field ctypes access costs
+        # microseconds per tensor, which adds up at 20,000 tensors)
+        raw = np.frombuffer(arr, dtype=_TENSOR_INFO, count=n.value)
+        names = [C.string_at(p).decode() for p in raw["name"].tolist()]
+        return [Tensor(nm, CODE_DTYPE[dt], tuple(sh[:nd]), off, nb)
+                for nm, dt, nd, sh, off, nb in zip(names, raw["dtype"].tolist(), raw["ndim"].tolist(),
+                                                   raw["shape"].tolist(), raw["offset"].tolist(),
+                                                   raw["nbytes"].tolist())]
 
     def find(self, name: str) -> Tensor:
         t = TensorInfo()
@@ -326,6 +345,36 @@ class Checkpoint:
     def load_into(self, buf, stream=None) -> None:
         """Load into a uint8 torch tensor on the handle's device."""
         self.load(buf.data_ptr(), buf.numel(), stream)
+
+    def load_with_views(self, buf, stream=None, after_load: Optional[Callable[[], None]] = None):
+        """Load into ``buf`` while this thread builds the tensor views
+        (``sllm_load`` runs on a helper thread; ctypes releases the GIL during
+        the call).  ``after_load`` runs on that thread once the load is
+        enqueued.  Returns ``{name: view}``; the data are ready once
+        ``stream`` has been synchronized."""
+        err: List[BaseException] = []
+
+        def run():
+            try:
+                self.load_into(buf, stream)
+                if after_load is not None:
+                    after_load()
+            except BaseException as e:  # re-raised on the calling thread
+                err.append(e)
+
+        th = threading.Thread(target=run, name="sllm-load")
+        th.start()
+        view_err = None
+        try:
+            out = views(buf, self.tensors())
+        except BaseException as e:  # e.g. a buffer too small for the views
+            view_err = e
+        th.join()
+        if err:  # the load's own error says more (SLLM_E_RANGE for a short buffer)
+            raise err[0]
+        if view_err is not None:
+            raise view_err
+        return out
 
     def repack(self, src, dst, stream=None) -> None:
         check(lib().sllm_repack(self._h, src.data_ptr(), src.numel(), dst.data_ptr(), dst.numel(),
@@ -367,12 +416,17 @@ def views(buf, tensors: Sequence[Tensor]) -> Dict[str, object]:
         if base is None:
             base = buf[: (buf.numel() // isz) * isz].view(tdt[t.dtype])
             typed[t.dtype] = base
-        stride, acc = [], 1
-        for d in reversed(t.shape):
-            stride.append(acc)
-            acc *= max(int(d), 1)
-        out[t.name] = base.as_strided(t.shape, tuple(reversed(stride)), t.offset // isz)
+        out[t.name] = base.as_strided(t.shape, _contiguous_strides(t.shape), t.offset // isz)
     return out
+
+
+@functools.lru_cache(maxsize=4096)
+def _contiguous_strides(shape: Tuple[int, ...]) -> Tuple[int, ...]:
+    stride, acc = [], 1
+    for d in reversed(shape):
+        stride.append(acc)
+        acc *= max(int(d), 1)
+    return tuple(reversed(stride))
 
 
 def load(ckpt_dir: str, device: int = 0, stream=None, pool: Optional[Pool] = None, **opts):
@@ -384,8 +438,7 @@ def load(ckpt_dir: str, device: int = 0, stream=None, pool: Optional[Pool] = Non
     with Checkpoint(ckpt_dir, device=device, pool=pool, **opts) as ck:
         buf = torch.empty(max(ck.total_bytes, 1), dtype=torch.uint8, device=f"cuda:{device}")
         s = stream if stream is not None else torch.cuda.current_stream(device)
-        ck.load_into(buf, s)
-        out = views(buf, ck.tensors())
+        out = ck.load_with_views(buf, s)
         s.synchronize()
     return buf, out
 

@@ -469,3 +469,35 @@ def test_offsets_scan_20000_tensors(torch_cuda, tmp_path, A2):
     with binding.Checkpoint(d, dev_alignment=A2, chunk_size=1 << 20) as ck:
         assert [t.offset for t in ck.tensors()] == d2 and ck.total_bytes == T2
         assert_same(run_load(torch, ck, len(want)), want, f"A2={A2}")
+
+
+@pytest.mark.parametrize("cached", [True, False])
+def test_load_with_views(torch_cuda, opt125m, cached):
+    """Views built while the load runs on a helper thread hold every
+    tensor's bytes once the stream is synchronized, and a load error raised
+    on that thread reaches the caller."""
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    pool = binding.Pool(spec.chunk_size, 32) if cached else None
+    try:
+        if pool:
+            pool.cache(d)
+        with binding.Checkpoint(d, pool=pool) as ck:
+            buf = torch.full((ck.total_bytes,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+            s = torch.cuda.Stream()
+            marks = []
+            views = ck.load_with_views(buf, s, after_load=lambda: marks.append(1))
+            s.synchronize()
+            assert marks == [1] and len(views) == len(tensors)
+            for (name, dt, shape, data) in tensors:
+                v = views[name]
+                assert tuple(v.shape) == tuple(shape)
+                assert v.contiguous().view(torch.uint8).cpu().numpy().tobytes() == data.tobytes(), name
+            small = torch.empty(ck.total_bytes - 1, dtype=torch.uint8, device="cuda:0")
+            with pytest.raises(binding.SllmError) as e:
+                ck.load_with_views(small, s)
+            assert e.value.code == -6
+    finally:
+        if pool:
+            pool.evict(d)
+            pool.close()
