@@ -427,7 +427,8 @@ def main():
     ap.add_argument("--dev-alignment", type=int, default=0,
                     help="load into a device layout with this alignment (K1-scatter, or copy engine + K2)")
     ap.add_argument("--io-threads", type=int, default=8)
-    ap.add_argument("--ring-slots", type=int, default=32)
+    ap.add_argument("--ring-slots", type=int, default=0,
+                    help="pinned ring slots for streamed regimes (default: 1 GiB of slots, at least 16)")
     ap.add_argument("--dir", default=None, help="where the converted checkpoint lives")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle reading")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -476,6 +477,8 @@ def main():
     log(f"measured peaks: pinned->HBM copy {h2d_peak} GB/s, HBM copy {hbm_peak} GB/s")
 
     C = args.chunk_size or spec.chunk_size
+    if not args.ring_slots:
+        args.ring_slots = max(16, (1 << 30) // C)
     with binding.Checkpoint(d, index_only=True, dev_alignment=args.dev_alignment) as probe:
         T = probe.total_bytes
     with binding.Checkpoint(d, index_only=True) as probe:

@@ -13,6 +13,7 @@
 #include <atomic>
 #include <chrono>
 #include <condition_variable>
+#include <cstdlib>
 #include <cstring>
 #include <deque>
 #include <mutex>
@@ -203,7 +204,15 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
 // that event has completed, polling in-flight batches in order and blocking
 // on the oldest only when every slot is on the GPU.  Batches still in flight
 // when the load returns are reclaimed at the start of the next one.
-constexpr uint64_t kBatchTargetBytes = 16ull << 20;
+// Bytes a streamed gather batch waits to collect (SLLM_BATCH_TARGET_MB,
+// default 16; 0 launches whatever is ready).
+uint64_t batch_target_bytes() {
+    const char* s = std::getenv("SLLM_BATCH_TARGET_MB");
+    if (!s || !*s) return 16ull << 20;
+    char* end = nullptr;
+    const long v = std::strtol(s, &end, 10);
+    return (end && *end == '\0' && v >= 0) ? (uint64_t)v << 20 : 16ull << 20;
+}
 
 int32_t reclaim_all(sllm_ckpt* h) {
     for (const InFlight& b : h->inflight) SLLM_HIP(hipEventSynchronize(b.ev));
@@ -320,8 +329,8 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             : 1;
     // a short batch is held back while the GPU still has two batches queued
     // and readers are filling slots, so that launches carry about
-    // kBatchTargetBytes each instead of whatever chunks arrived last
-    const uint64_t target = std::min<uint64_t>(max_batch, std::max<uint64_t>(1, kBatchTargetBytes / C));
+    // batch_target_bytes() each instead of whatever chunks arrived last
+    const uint64_t target = std::min<uint64_t>(max_batch, std::max<uint64_t>(1, batch_target_bytes() / C));
     std::vector<std::pair<uint64_t, uint32_t>> batch;
     batch.reserve(max_batch);
     double wait_s = 0;

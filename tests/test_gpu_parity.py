@@ -471,12 +471,14 @@ def test_offsets_scan_20000_tensors(torch_cuda, tmp_path, A2):
         assert_same(run_load(torch, ck, len(want)), want, f"A2={A2}")
 
 
+@pytest.mark.parametrize("threaded", [True, False])
 @pytest.mark.parametrize("cached", [True, False])
-def test_load_with_views(torch_cuda, opt125m, cached):
-    """Views built while the load runs on a helper thread hold every
-    tensor's bytes once the stream is synchronized, and a load error raised
-    on that thread reaches the caller."""
+def test_load_with_views(torch_cuda, opt125m, cached, threaded, monkeypatch):
+    """Views built while the load runs on a helper thread (or after it, for
+    few tensors) hold every tensor's bytes once the stream is synchronized,
+    and a load error reaches the caller."""
     torch = torch_cuda
+    monkeypatch.setattr(binding, "_THREADED_VIEWS_MIN", 0 if threaded else 1 << 30)
     spec, tensors, d = opt125m
     pool = binding.Pool(spec.chunk_size, 32) if cached else None
     try:
