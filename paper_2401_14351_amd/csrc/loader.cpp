@@ -40,6 +40,7 @@ struct Slot {
 struct InFlight {
     hipEvent_t ev = nullptr;
     std::vector<uint32_t> slots;
+    uint64_t bytes = 0;  // partition bytes the batch moves
 };
 
 }  // namespace
@@ -205,13 +206,14 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
 // on the oldest only when every slot is on the GPU.  Batches still in flight
 // when the load returns are reclaimed at the start of the next one.
 // Bytes a streamed gather batch waits to collect (SLLM_BATCH_TARGET_MB,
-// default 16; 0 launches whatever is ready).
+// default 64; 0 launches whatever is ready).
 uint64_t batch_target_bytes() {
+    constexpr uint64_t kDefault = 64ull << 20;
     const char* s = std::getenv("SLLM_BATCH_TARGET_MB");
-    if (!s || !*s) return 16ull << 20;
+    if (!s || !*s) return kDefault;
     char* end = nullptr;
     const long v = std::strtol(s, &end, 10);
-    return (end && *end == '\0' && v >= 0) ? (uint64_t)v << 20 : 16ull << 20;
+    return (end && *end == '\0' && v >= 0) ? (uint64_t)v << 20 : kDefault;
 }
 
 int32_t reclaim_all(sllm_ckpt* h) {
@@ -327,10 +329,16 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         (h->engine == SLLM_ENGINE_KERNEL && !h->dev_align)
             ? std::max<uint32_t>(1, std::min<uint32_t>(kGatherBatch, (uint32_t)h->slots.size() / 4))
             : 1;
-    // a short batch is held back while the GPU still has two batches queued
-    // and readers are filling slots, so that launches carry about
-    // batch_target_bytes() each instead of whatever chunks arrived last
+    // a short batch is held back while the GPU still has at least a full
+    // batch's bytes queued and readers are filling slots, so that launches
+    // carry about batch_target_bytes() each instead of whatever chunks
+    // arrived last (a gather launch ramps up and drains at its ends)
     const uint64_t target = std::min<uint64_t>(max_batch, std::max<uint64_t>(1, batch_target_bytes() / C));
+    auto queued_bytes = [&] {
+        uint64_t b = 0;
+        for (const InFlight& f : h->inflight) b += f.bytes;
+        return b;
+    };
     std::vector<std::pair<uint64_t, uint32_t>> batch;
     batch.reserve(max_batch);
     double wait_s = 0;
@@ -351,13 +359,16 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
                     cv_ready.wait_for(lk, std::chrono::microseconds(200), [&] { return stop || !ready_q.empty(); });
             }
             const uint64_t fill = std::min<uint64_t>(target, n - moved);
-            if (!wait_gpu && !stop && ready_q.size() < fill && h->inflight.size() >= 2 &&
-                (reading > 0 || !free_q.empty()))
-                cv_ready.wait_for(lk, std::chrono::microseconds(100),
+            bool hold = false;
+            if (!wait_gpu && !stop && ready_q.size() < fill && (reading > 0 || !free_q.empty()) &&
+                queued_bytes() >= target * C) {
+                cv_ready.wait_for(lk, std::chrono::microseconds(50),
                                   [&] { return stop || ready_q.size() >= fill; });
+                hold = !stop && ready_q.size() < fill;  // still short: reclaim, then look again
+            }
             wait_s += now_s() - w0;
             if (stop && ready_q.empty()) break;  // a reader failed
-            while (!ready_q.empty() && batch.size() < max_batch) {
+            while (!hold && !ready_q.empty() && batch.size() < max_batch) {
                 batch.push_back(ready_q.front());
                 ready_q.pop_front();
             }
@@ -388,7 +399,10 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             hipError_t e = hipEventRecord(f.ev, st);
             if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
         }
-        for (const auto& item : batch) f.slots.push_back(item.second);
+        for (const auto& item : batch) {
+            f.slots.push_back(item.second);
+            f.bytes += std::min(C, T - item.first * C);
+        }
         if (rc == SLLM_OK) {
             h->inflight.push_back(std::move(f));
         } else {  // nothing of this batch reached the GPU: its slots are free
