@@ -410,6 +410,25 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
                                "io_threads": 8, "ring_slots": 16, "read_wait_s": round(st["read_wait_s"], 3),
                                "device": block_device(d)}
     log("file ring:", out["file_direct_ring"])
+    # the tiers in one pass: a first load straight from the file (O_DIRECT)
+    # that leaves the partition cached in the pool (SLLM_OPEN_CACHE), then a
+    # load of the same handle from that cache
+    pool.evict(d)
+    t0 = time.perf_counter()
+    with binding.Checkpoint(d, pool=pool, engine=engine, cache=True, direct_io=True, io_threads=8) as ck:
+        ck.load_into(buf, stream)
+        stream.synchronize()
+        t1 = time.perf_counter()
+        first = ck.stats()
+        ck.load_into(buf, stream)
+        stream.synchronize()
+        t2 = time.perf_counter()
+        second = ck.stats()
+    out["file_direct_then_cached"] = {
+        "first_GBps": round(T / (t1 - t0) / 1e9, 3), "first_s": round(t1 - t0, 3),
+        "first_from_cache": int(first["from_cache"]), "second_GBps": round(T / (t2 - t1) / 1e9, 3),
+        "second_from_cache": int(second["from_cache"]), "cached_after": pool.info()["cached_checkpoints"]}
+    log("file then cached:", out["file_direct_then_cached"])
     return out
 
 

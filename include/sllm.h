@@ -174,6 +174,16 @@ int32_t sllm_pool_evict(sllm_pool* pool, const char* dir);
                                    file, pool or device work; for processes
                                    that view a buffer another process loaded
                                    (sllm_load then returns SLLM_E_INVAL)      */
+#define SLLM_OPEN_CACHE     8u  /* keep what the first load reads: it streams
+                                   the file (storage -> pinned -> HBM,
+                                   pipelined) into ceil(T/C) chunks of
+                                   opts->pool, one per chunk, and once it has
+                                   succeeded those chunks become the pool's
+                                   cached copy of the checkpoint (the DRAM
+                                   tier, Sec. 4.2), as after sllm_pool_cache.
+                                   Needs a pool whose chunk size is C; NOMEM
+                                   if it lacks free chunks.  No effect when
+                                   the checkpoint is cached already.        */
 
 typedef struct sllm_open_opts {
     uint64_t   chunk_size;     /* C for reads from the file; 0 = pool's chunk

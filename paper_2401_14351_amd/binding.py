@@ -31,6 +31,7 @@ ENGINE = {"kernel": 0, "sdma": 1}
 OPEN_DIRECT_IO = 1
 OPEN_TIMING = 2
 OPEN_INDEX_ONLY = 4
+OPEN_CACHE = 8
 CONVERT_FSYNC = 1
 MAX_NDIM = 8
 
@@ -308,9 +309,12 @@ class Checkpoint:
 
     def __init__(self, ckpt_dir: str, device: int = 0, pool: Optional[Pool] = None, chunk_size: int = 0,
                  dev_alignment: int = 0, io_threads: int = 4, n_streams: int = 2, ring_slots: int = 0,
-                 engine: str = "kernel", direct_io: bool = False, timing: bool = False, index_only: bool = False):
+                 engine: str = "kernel", direct_io: bool = False, timing: bool = False, index_only: bool = False,
+                 cache: bool = False):
+        """cache=True (SLLM_OPEN_CACHE): the first load streams into one chunk
+        of ``pool`` per partition chunk and leaves the checkpoint cached there."""
         flags = (OPEN_DIRECT_IO if direct_io else 0) | (OPEN_TIMING if timing else 0) | \
-            (OPEN_INDEX_ONLY if index_only else 0)
+            (OPEN_INDEX_ONLY if index_only else 0) | (OPEN_CACHE if cache else 0)
         opts = OpenOpts(chunk_size, dev_alignment, pool.handle if pool else None, io_threads, n_streams,
                         ring_slots, ENGINE[engine], flags, device)
         self._h = C.c_void_p()

@@ -67,6 +67,8 @@ struct sllm_ckpt {
     hipEvent_t fork_ev = nullptr, t0_ev = nullptr, t1_ev = nullptr;
     bool timed = false;             // t0/t1 bracket the last load
     DeviceLayout layout;            // device tables for A2 layouts
+    bool keep = false;              // SLLM_OPEN_CACHE: chunk k streams into slot k, kept afterwards
+    const uint8_t** keep_table = nullptr;  // device table of the kept slots, until the pool adopts it
     std::atomic<bool> busy{false};
     sllm_stats stats{};
 };
@@ -88,6 +90,7 @@ void release(sllm_ckpt* h) {
         for (hipStream_t s : h->streams) (void)hipStreamDestroy(s);
         device_layout_free(&h->layout);
     }
+    if (h->keep_table) pool_free_table(h->pool, h->keep_table);
     if (h->pool) {
         std::lock_guard<std::mutex> g(h->pool->mu);
         if (!h->slot_ids.empty()) pool_give(h->pool, h->slot_ids);
@@ -222,6 +225,23 @@ int32_t reclaim_all(sllm_ckpt* h) {
     return SLLM_OK;
 }
 
+// After a successful streamed load with kept slots, hand them to the pool as
+// its cached copy of the checkpoint; the handle then loads from the cache.
+// If another handle cached the same file meanwhile, the slots stay with this
+// handle and its loads keep streaming.
+void adopt_kept(sllm_ckpt* h) {
+    CacheEntry* e = nullptr;
+    if (pool_adopt(h->pool, h->dir.c_str(), h->file, h->ix.total, h->slot_ids, h->keep_table, 1, &e) != SLLM_OK) {
+        log_msg(1, "%s was cached by another handle; this one keeps streaming", h->dir.c_str());
+        clear_error();
+        return;
+    }
+    h->cached = e;
+    h->slot_ids.clear();  // owned by the cache entry now
+    h->keep_table = nullptr;
+    h->keep = false;
+}
+
 int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     const uint64_t C = h->chunk, T = h->ix.total;
     const uint64_t n = ceil_div(T, C);
@@ -234,7 +254,8 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     std::condition_variable cv_free, cv_ready;
     std::deque<uint32_t> free_q;
     std::deque<std::pair<uint64_t, uint32_t>> ready_q;
-    for (uint32_t i = 0; i < h->slots.size(); ++i) free_q.push_back(i);
+    if (!h->keep)
+        for (uint32_t i = 0; i < h->slots.size(); ++i) free_q.push_back(i);
     std::atomic<uint64_t> next{0};
     uint32_t reading = 0;  // slots held by readers
     bool stop = false;
@@ -261,11 +282,16 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             {
                 const double w0 = now_s();
                 std::unique_lock<std::mutex> lk(mu);
-                cv_free.wait(lk, [&] { return stop || !free_q.empty(); });
-                starved_ns += (uint64_t)((now_s() - w0) * 1e9);
-                if (stop) return;
-                si = free_q.front();
-                free_q.pop_front();
+                if (h->keep) {  // chunk k has a slot of its own
+                    if (stop) return;
+                    si = (uint32_t)k;
+                } else {
+                    cv_free.wait(lk, [&] { return stop || !free_q.empty(); });
+                    starved_ns += (uint64_t)((now_s() - w0) * 1e9);
+                    if (stop) return;
+                    si = free_q.front();
+                    free_q.pop_front();
+                }
                 ++reading;
             }
             const uint64_t off = k * C, len = std::min(C, read_end - off);
@@ -276,7 +302,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             std::lock_guard<std::mutex> g(mu);
             --reading;
             if (st != SLLM_OK) {
-                free_q.push_back(si);
+                if (!h->keep) free_q.push_back(si);
                 set_error(st);
                 return;
             }
@@ -311,7 +337,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             block = false;
             if (e == hipErrorNotReady) break;
             if (e != hipSuccess) return fail(SLLM_E_HIP, "waiting for a batch: %s", hipGetErrorString(e));
-            {
+            if (!h->keep) {  // kept slots are not refilled
                 std::lock_guard<std::mutex> g(mu);
                 for (uint32_t si : h->inflight.front().slots) free_q.push_back(si);
             }
@@ -352,16 +378,18 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         {
             const double w0 = now_s();
             std::unique_lock<std::mutex> lk(mu);
+            // readers are reading, or will start on a free slot (a chunk of
+            // their own when slots are kept)
+            const bool readers_busy = reading > 0 || (h->keep ? next.load() < n : !free_q.empty());
             if (ready_q.empty() && !stop) {
-                if (free_q.empty() && reading == 0 && !h->inflight.empty())
+                if (!readers_busy && !h->inflight.empty())
                     wait_gpu = true;  // every slot is on the GPU
                 else
                     cv_ready.wait_for(lk, std::chrono::microseconds(200), [&] { return stop || !ready_q.empty(); });
             }
             const uint64_t fill = std::min<uint64_t>(target, n - moved);
             bool hold = false;
-            if (!wait_gpu && !stop && ready_q.size() < fill && (reading > 0 || !free_q.empty()) &&
-                queued_bytes() >= target * C) {
+            if (!wait_gpu && !stop && ready_q.size() < fill && readers_busy && queued_bytes() >= target * C) {
                 cv_ready.wait_for(lk, std::chrono::microseconds(50),
                                   [&] { return stop || ready_q.size() >= fill; });
                 hold = !stop && ready_q.size() < fill;  // still short: reclaim, then look again
@@ -432,7 +460,9 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         h->inflight.clear();
         return fail(err, "%s", err_msg.c_str());
     }
-    return join_streams(h, user);
+    SLLM_TRY(join_streams(h, user));
+    if (h->keep) adopt_kept(h);
+    return SLLM_OK;
 }
 
 }  // namespace
@@ -445,8 +475,10 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
     sllm_open_opts o{};
     if (opts) o = *opts;
     if (o.engine != SLLM_ENGINE_KERNEL && o.engine != SLLM_ENGINE_SDMA) return fail(SLLM_E_INVAL, "unknown engine %u", o.engine);
-    if (o.flags & ~(SLLM_OPEN_DIRECT_IO | SLLM_OPEN_TIMING | SLLM_OPEN_INDEX_ONLY))
+    if (o.flags & ~(SLLM_OPEN_DIRECT_IO | SLLM_OPEN_TIMING | SLLM_OPEN_INDEX_ONLY | SLLM_OPEN_CACHE))
         return fail(SLLM_E_INVAL, "unknown flags 0x%x", o.flags);
+    if ((o.flags & SLLM_OPEN_CACHE) && (!o.pool || (o.flags & SLLM_OPEN_INDEX_ONLY)))
+        return fail(SLLM_E_INVAL, "SLLM_OPEN_CACHE needs a pool and a data file");
     if (o.dev_alignment && (!is_pow2(o.dev_alignment) || o.dev_alignment < 16))
         return fail(SLLM_E_INVAL, "device alignment %llu is not a power of two >= 16", (unsigned long long)o.dev_alignment);
     if (o.pool && o.pool->device != o.device)
@@ -513,11 +545,14 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
             h->cached = pool_find(h->pool, h->file);
             if (h->cached) ++h->cached->refs;
             h->chunk = h->cached ? h->pool->chunk : (o.chunk_size ? o.chunk_size : h->pool->chunk);
-            if (h->cached && o.chunk_size && o.chunk_size != h->pool->chunk)
-                st = fail(SLLM_E_INVAL, "cached partition uses the pool's chunk size %llu", (unsigned long long)h->pool->chunk);
+            h->keep = !h->cached && (o.flags & SLLM_OPEN_CACHE);
+            if ((h->cached || h->keep) && o.chunk_size && o.chunk_size != h->pool->chunk)
+                st = fail(SLLM_E_INVAL, "cached partitions use the pool's chunk size %llu", (unsigned long long)h->pool->chunk);
             else if (h->chunk > h->pool->chunk)
                 st = fail(SLLM_E_INVAL, "chunk size %llu exceeds the pool's %llu", (unsigned long long)h->chunk,
                           (unsigned long long)h->pool->chunk);
+            else if (h->keep)  // one chunk of the pool per chunk of the partition
+                st = pool_take(h->pool, ceil_div(h->ix.total, h->chunk), &h->slot_ids);
             else if (!h->cached)
                 st = pool_take(h->pool, h->ring_slots, &h->slot_ids);
         }
@@ -567,6 +602,10 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
         s.host = h->pool->host[s.id];
         s.mapped = h->pool->mapped[s.id];
         if (!hip_ok(hipEventCreateWithFlags(&s.done, hipEventDisableTiming), "hipEventCreateWithFlags")) return bail(SLLM_E_HIP);
+    }
+    if (h->keep) {
+        st = pool_chunk_table(h->pool, h->slot_ids, &h->keep_table);
+        if (st != SLLM_OK) return bail(st);
     }
     if (h->dev_align) {
         std::vector<uint64_t> file_off(nt), sizes(nt);

@@ -109,6 +109,53 @@ int32_t parallel_chunks(uint64_t n, uint32_t threads, int device, const std::fun
     return SLLM_OK;
 }
 
+std::string canonical_dir(const char* dir) {
+    char buf[PATH_MAX];
+    return ::realpath(dir, buf) ? std::string(buf) : std::string(dir);
+}
+
+int32_t pool_chunk_table(sllm_pool* p, const std::vector<uint32_t>& ids, const uint8_t*** out) {
+    *out = nullptr;
+    if (ids.empty()) return SLLM_OK;
+    DeviceGuard guard(p->device);
+    std::vector<const uint8_t*> table(ids.size());
+    for (size_t k = 0; k < ids.size(); ++k) table[k] = p->mapped[ids[k]];
+    const uint8_t** d = nullptr;
+    hipError_t he = hipMalloc(reinterpret_cast<void**>(&d), table.size() * sizeof(void*));
+    if (he == hipSuccess) he = hipMemcpy(d, table.data(), table.size() * sizeof(void*), hipMemcpyHostToDevice);
+    if (he != hipSuccess) {
+        if (d) (void)hipFree(d);
+        return fail(SLLM_E_HIP, "chunk table upload failed: %s", hipGetErrorString(he));
+    }
+    *out = d;
+    return SLLM_OK;
+}
+
+void pool_free_table(sllm_pool* p, const uint8_t** d_table) {
+    if (!d_table) return;
+    DeviceGuard guard(p->device);
+    (void)hipFree(const_cast<uint8_t**>(d_table));
+}
+
+int32_t pool_adopt(sllm_pool* p, const char* dir, const DataFile& f, uint64_t total, const std::vector<uint32_t>& ids,
+                   const uint8_t** d_table, int refs, CacheEntry** out) {
+    auto e = std::make_unique<CacheEntry>();
+    e->dir = canonical_dir(dir);
+    e->dev = f.dev;
+    e->ino = f.ino;
+    e->size = f.size;
+    e->mtime_ns = f.mtime_ns;
+    e->total = total;
+    e->chunks = ids;
+    e->d_table = d_table;
+    e->refs = refs;
+    std::lock_guard<std::mutex> g(p->mu);
+    if (pool_find(p, f)) return fail(SLLM_E_BUSY, "%s is already cached", dir);
+    if (out) *out = e.get();
+    p->cache.push_back(std::move(e));
+    return SLLM_OK;
+}
+
 }  // namespace sllm
 
 namespace {
@@ -149,11 +196,6 @@ void prefault(const std::vector<void*>& arenas, uint64_t arena_bytes_last, uint6
         for (uint64_t o = 0; o < pieces[k].n; o += 4096) p[o] = 0;
         return SLLM_OK;
     });
-}
-
-std::string canonical(const char* dir) {
-    char buf[PATH_MAX];
-    return ::realpath(dir, buf) ? std::string(buf) : std::string(dir);
 }
 
 }  // namespace
@@ -280,41 +322,21 @@ extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_th
         give_back();
         return st;
     }
-    auto e = std::make_unique<CacheEntry>();
-    e->dir = canonical(dir);
-    e->dev = f.dev;
-    e->ino = f.ino;
-    e->size = f.size;
-    e->mtime_ns = f.mtime_ns;
-    e->total = ix.total;
-    e->chunks = ids;
-    if (n) {
-        DeviceGuard guard(p->device);
-        std::vector<const uint8_t*> table(n);
-        for (uint64_t k = 0; k < n; ++k) table[k] = p->mapped[ids[k]];
-        hipError_t he = hipMalloc(reinterpret_cast<void**>(&e->d_table), n * sizeof(void*));
-        if (he == hipSuccess) he = hipMemcpy(e->d_table, table.data(), n * sizeof(void*), hipMemcpyHostToDevice);
-        if (he != hipSuccess) {
-            if (e->d_table) (void)hipFree(e->d_table);
-            give_back();
-            return fail(SLLM_E_HIP, "chunk table upload failed: %s", hipGetErrorString(he));
-        }
+    const uint8_t** d_table = nullptr;
+    st = pool_chunk_table(p, ids, &d_table);
+    if (st == SLLM_OK) st = pool_adopt(p, dir, f, ix.total, ids, d_table, 0, nullptr);
+    if (st != SLLM_OK) {  // nothing was adopted: the chunks and the table are still ours
+        pool_free_table(p, d_table);
+        give_back();
+        return st;
     }
-    std::lock_guard<std::mutex> g(p->mu);
-    if (pool_find(p, f)) {  // cached concurrently by another thread
-        DeviceGuard guard(p->device);
-        if (e->d_table) (void)hipFree(e->d_table);
-        pool_give(p, ids);
-        return fail(SLLM_E_BUSY, "%s is already cached", dir);
-    }
-    p->cache.push_back(std::move(e));
     return SLLM_OK;
 } SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_pool_evict(sllm_pool* p, const char* dir) try {
     clear_error();
     if (!p || !dir) return fail(SLLM_E_INVAL, "pool and dir must be non-NULL");
-    const std::string canon = canonical(dir);
+    const std::string canon = canonical_dir(dir);
     struct stat st;
     const bool have = ::stat((std::string(dir) + "/" + kDataName).c_str(), &st) == 0;
     std::lock_guard<std::mutex> g(p->mu);

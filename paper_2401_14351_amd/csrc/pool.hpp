@@ -49,6 +49,23 @@ void pool_give(sllm_pool* p, const std::vector<uint32_t>& ids);
 // The cache entry for this data file, or null (caller holds p->mu).
 CacheEntry* pool_find(sllm_pool* p, const DataFile& f);
 
+// A device array holding the mapped address of chunk ids[k] at k (null for
+// no ids); free it with pool_free_table unless a cache entry adopts it.
+int32_t pool_chunk_table(sllm_pool* p, const std::vector<uint32_t>& ids, const uint8_t*** out);
+void pool_free_table(sllm_pool* p, const uint8_t** d_table);
+
+// Register chunks `ids` (chunk k of the partition of data file `f` in
+// ids[k]) and their device table as the pool's cached copy of checkpoint
+// `dir`, with `refs` handles already loading from it.  On success the entry
+// owns the chunks and the table (*out, if given, points to it); BUSY if that
+// file is cached already, and then nothing is taken.  Caller must not hold
+// p->mu.
+int32_t pool_adopt(sllm_pool* p, const char* dir, const DataFile& f, uint64_t total, const std::vector<uint32_t>& ids,
+                   const uint8_t** d_table, int refs, CacheEntry** out);
+
+// realpath of dir, or dir itself if that fails.
+std::string canonical_dir(const char* dir);
+
 }  // namespace sllm
 
 namespace sllm {

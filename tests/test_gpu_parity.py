@@ -503,3 +503,75 @@ def test_load_with_views(torch_cuda, opt125m, cached, threaded, monkeypatch):
         if pool:
             pool.evict(d)
             pool.close()
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("direct", [False, True])
+def test_open_cache_keeps_first_load(torch_cuda, opt125m, engine, direct):
+    """SLLM_OPEN_CACHE: the first load streams the file into one pool chunk
+    per partition chunk and leaves them as the pool's cached copy; the next
+    load of the handle and a new handle's load come from that cache, every
+    load byte-identical; eviction waits for the handle to close."""
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, index = expected(tensors, spec.alignment)
+    n = -(-index.total_bytes // spec.chunk_size)
+    with binding.Pool(spec.chunk_size, n + 3) as pool:
+        with binding.Checkpoint(d, pool=pool, engine=engine, cache=True, direct_io=direct, io_threads=4) as ck:
+            info = pool.info()
+            assert info["free_chunks"] == 3 and info["cached_checkpoints"] == 0
+            assert_same(run_load(torch, ck, len(want)), want, "first load")
+            st = ck.stats()
+            assert st["from_cache"] == 0 and st["bytes_read"] >= index.total_bytes
+            info = pool.info()
+            assert info["cached_checkpoints"] == 1 and info["free_chunks"] == 3
+            with pytest.raises(binding.SllmError) as ei:
+                pool.evict(d)
+            assert ei.value.code == -7
+            assert_same(run_load(torch, ck, len(want)), want, "second load")
+            assert ck.stats()["from_cache"] == 1
+            with binding.Checkpoint(d, pool=pool, engine=engine, cache=True) as ck2:
+                assert_same(run_load(torch, ck2, len(want)), want, "another handle")
+                assert ck2.stats()["from_cache"] == 1
+        pool.evict(d)
+        assert pool.info()["free_chunks"] == n + 3
+
+
+def test_open_cache_rules(torch_cuda, opt125m, tmp_path):
+    """SLLM_OPEN_CACHE needs a pool with room and the pool's chunk size; a
+    failed first load caches nothing and gives every chunk back at close."""
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, index = expected(tensors, spec.alignment)
+    n = -(-index.total_bytes // spec.chunk_size)
+    with pytest.raises(binding.SllmError) as ei:
+        binding.Checkpoint(d, cache=True)
+    assert ei.value.code == -1
+    with binding.Pool(spec.chunk_size, n - 1) as small:
+        with pytest.raises(binding.SllmError) as ei:
+            binding.Checkpoint(d, pool=small, cache=True)
+        assert ei.value.code == -4
+        assert small.info()["free_chunks"] == n - 1
+    with binding.Pool(spec.chunk_size, n) as pool:
+        with pytest.raises(binding.SllmError) as ei:
+            binding.Checkpoint(d, pool=pool, cache=True, chunk_size=spec.chunk_size // 2)
+        assert ei.value.code == -1
+        # a read failure in the first load: nothing is cached
+        d2 = tmp_path / "ck"
+        binding.convert(iter(tensors), str(d2), spec.alignment, spec.chunk_size)
+        path = d2 / "sllm.part0"
+        full = open(path, "rb").read()
+        with binding.Checkpoint(str(d2), pool=pool, cache=True) as ck:
+            with open(path, "r+b") as f:
+                f.truncate(len(full) // 2)
+            buf = torch.empty(len(want), dtype=torch.uint8, device="cuda:0")
+            with pytest.raises(binding.SllmError) as ei:
+                ck.load_into(buf)
+            assert ei.value.code == -2
+            assert pool.info()["cached_checkpoints"] == 0
+            with open(path, "wb") as f:
+                f.write(full)
+            assert_same(run_load(torch, ck, len(want)), want, "after restoring the file")
+            assert pool.info()["cached_checkpoints"] == 1
+        pool.evict(str(d2))
+        assert pool.info()["free_chunks"] == n
