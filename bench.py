@@ -522,7 +522,7 @@ def main():
 
     ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ready, loads = [], []
+    ready, loads, open_s = [], [], []
 
     def step(i=None):
         t_open = time.perf_counter()
@@ -535,6 +535,7 @@ def main():
         stream.synchronize()
         t_end = time.perf_counter()
         last_stats.update(ck.stats())
+        open_s.append(last_stats["open_s"])
         ck.close()
         return t_end - t_open, t_end - t_load, views
 
@@ -609,6 +610,7 @@ def main():
         "time_to_ready_min_s": round(min(ready), 5),
         "load_GBps": round(T / statistics.median(loads) / 1e9, 3),
         "load_GBps_best": round(T / min(loads) / 1e9, 3),
+        "open_ms": round(statistics.median(open_s[-args.steps:]) * 1e3, 3),
         "roofline": {"bound": "pcie", "achieved": round(achieved, 3), "peak": PCIE_GEN5_X16_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PCIE_GEN5_X16_GBPS, 4),
                      "traffic": k1_counters["fetch_bytes_per_launch"] if k1_counters else None,

@@ -80,14 +80,17 @@ void release(sllm_ckpt* h) {
                           h->layout.d_off || h->layout.staging;
     if (used_hip) {
         DeviceGuard guard(h->device);
-        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
+        for (hipStream_t s : h->streams)
+            if (s) (void)hipStreamSynchronize(s);
         for (const InFlight& b : h->inflight) (void)hipEventSynchronize(b.ev);
         for (Slot& s : h->slots)
             if (s.done) (void)hipEventDestroy(s.done);
-        for (hipEvent_t e : h->join_ev) (void)hipEventDestroy(e);
+        for (hipEvent_t e : h->join_ev)
+            if (e) (void)hipEventDestroy(e);
         for (hipEvent_t e : {h->fork_ev, h->t0_ev, h->t1_ev})
             if (e) (void)hipEventDestroy(e);
-        for (hipStream_t s : h->streams) (void)hipStreamDestroy(s);
+        for (hipStream_t s : h->streams)
+            if (s) (void)hipStreamDestroy(s);
         device_layout_free(&h->layout);
     }
     if (h->keep_table) pool_free_table(h->pool, h->keep_table);
@@ -100,6 +103,21 @@ void release(sllm_ckpt* h) {
     if (h->own_pool) (void)sllm_pool_destroy(h->pool);
     close_data(&h->file);
     delete h;
+}
+
+// The copy streams and their fork/join events, created at the first load
+// that needs them (a cached load by the kernel engine runs on the caller's
+// stream alone, so opening such a handle creates no HIP objects).
+int32_t ensure_streams(sllm_ckpt* h) {
+    if (!h->streams.empty()) return SLLM_OK;
+    h->streams.assign(h->n_streams, nullptr);
+    h->join_ev.assign(h->n_streams, nullptr);
+    for (uint32_t i = 0; i < h->n_streams; ++i) {
+        SLLM_HIP(hipStreamCreateWithFlags(&h->streams[i], hipStreamNonBlocking));
+        SLLM_HIP(hipEventCreateWithFlags(&h->join_ev[i], hipEventDisableTiming));
+    }
+    SLLM_HIP(hipEventCreateWithFlags(&h->fork_ev, hipEventDisableTiming));
+    return SLLM_OK;
 }
 
 // Make the copy streams wait for work already queued on `user`.
@@ -172,6 +190,7 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         g.n_chunks = n;
         return launch_gather(g, user);
     }
+    SLLM_TRY(ensure_streams(h));
     SLLM_TRY(fork_streams(h, user));
     // merge chunks that are adjacent in host memory into one copy; with a
     // device layout a merged run goes to this stream's HBM staging chunk and
@@ -248,6 +267,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     const uint64_t read_end = h->file.direct ? h->ix.file_bytes : T;
     h->stats.n_chunks = n;
     SLLM_TRY(reclaim_all(h));
+    SLLM_TRY(ensure_streams(h));
     SLLM_TRY(fork_streams(h, user));
 
     std::mutex mu;
@@ -585,15 +605,8 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
         fail(SLLM_E_HIP, "%s failed: %s", what, hipGetErrorString(e));
         return false;
     };
-    h->streams.resize(h->n_streams, nullptr);
-    h->join_ev.resize(h->n_streams, nullptr);
-    for (uint32_t i = 0; i < h->n_streams; ++i) {
-        if (!hip_ok(hipStreamCreateWithFlags(&h->streams[i], hipStreamNonBlocking), "hipStreamCreateWithFlags") ||
-            !hip_ok(hipEventCreateWithFlags(&h->join_ev[i], hipEventDisableTiming), "hipEventCreateWithFlags"))
-            return bail(SLLM_E_HIP);
-    }
-    if (!hip_ok(hipEventCreateWithFlags(&h->fork_ev, hipEventDisableTiming), "hipEventCreateWithFlags") ||
-        !hip_ok(hipEventCreate(&h->t0_ev), "hipEventCreate") || !hip_ok(hipEventCreate(&h->t1_ev), "hipEventCreate"))
+    if ((o.flags & SLLM_OPEN_TIMING) &&
+        (!hip_ok(hipEventCreate(&h->t0_ev), "hipEventCreate") || !hip_ok(hipEventCreate(&h->t1_ev), "hipEventCreate")))
         return bail(SLLM_E_HIP);
     h->slots.resize(h->slot_ids.size());
     for (size_t i = 0; i < h->slot_ids.size(); ++i) {
