@@ -120,3 +120,153 @@ def test_stress_8g_file_and_device_layout(torch_cuda):
     check_zero_gaps(torch, direct, d2, sizes, T2)
     check_tensors(torch, spec, direct, d2)
     say("stress-8g: file and device layouts match")
+
+
+def sample(n, k, seed):
+    """k tensor indices drawn without replacement, plus the first and last."""
+    rng = np.random.default_rng(seed)
+    return sorted({0, n - 1, *rng.choice(n, size=min(k, n), replace=False).tolist()})
+
+
+def check_sampled_gaps(torch, buf, offsets, sizes, total, indices):
+    """The padding after each sampled tensor is zero."""
+    for i in indices:
+        a = offsets[i] + sizes[i]
+        b = offsets[i + 1] if i + 1 < len(offsets) else total
+        if b > a and int(buf[a:b].to(torch.int32).abs().sum()) != 0:
+            raise AssertionError(f"padding [{a}, {b}) after tensor {i} is not zero")
+
+
+def shm_dir(name):
+    base = "/dev/shm/sllm_test"
+    if not os.path.isdir("/dev/shm"):
+        pytest.skip("no /dev/shm")
+    return os.path.join(base, name)
+
+
+def converted_at(spec, d):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+
+    bench.ensure_checkpoint(spec, d)
+    return d
+
+
+@pytest.mark.parametrize("C_mib", [4, 16, 64])
+def test_llama2_13b_chunk_sizes(torch_cuda, C_mib):
+    """26.0 GB, 363 tensors, the chunk-size sweep: the partition cached in
+    4 / 16 / 64 MiB pool chunks and moved by one K1 launch; sampled tensors
+    against the generator, nothing written past T."""
+    torch = torch_cuda
+    spec = synth.llama2("13b")
+    d = converted(spec)
+    sizes = [t.nbytes for t in spec.tensors]
+    offsets, T = oracle.plan_layout(sizes, spec.alignment)
+    C = C_mib << 20
+    say("13b: C", C, "T", T)
+    with binding.Pool(C, -(-T // C)) as pool:
+        pool.cache(d, io_threads=8)
+        with binding.Checkpoint(d, pool=pool) as ck:
+            assert ck.total_bytes == T and [t.offset for t in ck.tensors()] == offsets
+            buf = torch.full((T + 4096,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+            ck.load_into(buf)
+            torch.cuda.synchronize()
+            assert ck.stats()["from_cache"] == 1
+        pool.evict(d)
+    assert bool((buf[T:] == SENTINEL).all())
+    idx = sample(len(sizes), 24, seed=C_mib)
+    check_sampled_gaps(torch, buf, offsets, sizes, T, idx)
+    check_tensors(torch, spec, buf, offsets, indices=idx)
+    del buf
+    torch.cuda.empty_cache()
+    say("13b: sampled tensors match")
+
+
+def test_llama2_13b_ring_4mib(torch_cuda):
+    """The 13B partition streamed from the file through a 1 GiB ring of
+    4 MiB slots (batched K1 launches); sampled tensors."""
+    torch = torch_cuda
+    spec = synth.llama2("13b")
+    d = converted(spec)
+    sizes = [t.nbytes for t in spec.tensors]
+    offsets, T = oracle.plan_layout(sizes, spec.alignment)
+    C = 4 << 20
+    with binding.Pool(C, 256) as pool:
+        with binding.Checkpoint(d, pool=pool, chunk_size=C, io_threads=8, ring_slots=256) as ck:
+            buf = torch.full((T + 4096,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+            ck.load_into(buf)
+            torch.cuda.synchronize()
+            st = ck.stats()
+            assert st["from_cache"] == 0 and st["n_launches"] < st["n_chunks"]
+    assert bool((buf[T:] == SENTINEL).all())
+    idx = sample(len(sizes), 24, seed=44)
+    check_sampled_gaps(torch, buf, offsets, sizes, T, idx)
+    check_tensors(torch, spec, buf, offsets, indices=idx)
+    del buf
+    torch.cuda.empty_cache()
+    say("13b ring: sampled tensors match")
+
+
+def test_llama2_70b_ring_from_shm(torch_cuda):
+    """137.95 GB, 723 tensors (more than the box's free disk, so the file
+    sits in /dev/shm): streamed through a 16 x 64 MiB ring by 16 readers, as
+    the bench runs it; sampled tensors."""
+    torch = torch_cuda
+    spec = synth.llama2("70b")
+    d = shm_dir(spec.name)
+    buf = None
+    try:
+        converted_at(spec, d)
+        sizes = [t.nbytes for t in spec.tensors]
+        offsets, T = oracle.plan_layout(sizes, spec.alignment)
+        say("70b: T", T)
+        with binding.Pool(spec.chunk_size, 16) as pool:
+            with binding.Checkpoint(d, pool=pool, io_threads=16, ring_slots=16) as ck:
+                assert ck.total_bytes == T
+                buf = torch.full((T + 4096,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+                ck.load_into(buf)
+                torch.cuda.synchronize()
+        assert bool((buf[T:] == SENTINEL).all())
+        idx = sample(len(sizes), 16, seed=70)
+        check_sampled_gaps(torch, buf, offsets, sizes, T, idx)
+        check_tensors(torch, spec, buf, offsets, indices=idx)
+        say("70b: sampled tensors match")
+    finally:
+        import shutil
+
+        shutil.rmtree(d, ignore_errors=True)
+        buf = None  # drop the image before handing its memory back
+        torch.cuda.empty_cache()
+
+
+def test_stress_full_ring_from_shm(torch_cuda):
+    """The full stress workload (20,000 tensors, all four dtypes, sizes
+    log-uniform over [256 B, 64 MiB], 4 KiB alignment, 1 MiB chunks: about
+    108 GB, in /dev/shm) streamed through a 1 GiB ring; sampled tensors and
+    the padding after them."""
+    torch = torch_cuda
+    spec = synth.config("stress")
+    d = shm_dir(spec.name)
+    buf = None
+    try:
+        converted_at(spec, d)
+        sizes = [t.nbytes for t in spec.tensors]
+        offsets, T = oracle.plan_layout(sizes, spec.alignment)
+        say("stress: n", len(sizes), "T", T)
+        with binding.Pool(spec.chunk_size, 1024) as pool:
+            with binding.Checkpoint(d, pool=pool, io_threads=8, ring_slots=1024) as ck:
+                assert ck.total_bytes == T and [t.offset for t in ck.tensors()] == offsets
+                buf = torch.full((T + 4096,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+                ck.load_into(buf)
+                torch.cuda.synchronize()
+        assert bool((buf[T:] == SENTINEL).all())
+        idx = sample(len(sizes), 64, seed=5)
+        check_sampled_gaps(torch, buf, offsets, sizes, T, idx)
+        check_tensors(torch, spec, buf, offsets, indices=idx)
+        say("stress: sampled tensors match")
+    finally:
+        import shutil
+
+        shutil.rmtree(d, ignore_errors=True)
+        buf = None  # drop the image before handing its memory back
+        torch.cuda.empty_cache()
