@@ -48,4 +48,13 @@ int32_t launch_scatter_window(const DeviceLayout& l, uint8_t* dst, const uint8_t
 int32_t launch_scatter_table(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* table, uint64_t chunk,
                              hipStream_t stream);
 
+// Up to this many chunks, each from its own slot, in one scatter launch.
+constexpr uint32_t kScatterBatch = 64;
+
+// Move the run of m (<= kScatterBatch) consecutive chunks k0 .. k0 + m - 1,
+// chunk k0 + j held at the device-visible host address srcs[j], into the
+// device image (the window [k0 C, min((k0 + m) C, T))).
+int32_t launch_scatter_run(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* srcs, uint64_t k0, uint32_t m,
+                           uint64_t chunk, hipStream_t stream);
+
 }  // namespace sllm

@@ -94,23 +94,38 @@ struct ScatterArgs {
     // ... or a table of chunks
     const uint8_t* const* table;  // partition byte x at table[x / chunk][x % chunk]
     uint64_t chunk;
+    // ... or a run of chunks passed inline (run_n > 0): byte x of chunk
+    // k = x / chunk at run_src[k - run_k0][x % chunk], for x in [x0, x1)
+    uint32_t run_n;
+    uint64_t run_k0;
+    const uint8_t* run_src[kScatterBatch];
     uint64_t total;        // T
     uint32_t vec_ok;       // 16-byte aligned source vectors are addressable as such
 };
 
+// Where a launch's source bytes are: one contiguous window, a device table
+// of chunks, or a run of chunks passed inline.  A kernel instance serves one
+// kind, so none of them pays for the others' addressing.
+enum SrcKind : int { kWindow = 0, kTable = 1, kRun = 2 };
+
+template <SrcKind K>
 struct Src {
     const ScatterArgs& a;
     __device__ __forceinline__ const uint8_t* at(uint64_t x) const {
-        if (a.table) {
+        if constexpr (K == kRun) {
+            const uint64_t k = x / a.chunk;
+            return a.run_src[k - a.run_k0] + (x - k * a.chunk);
+        } else if constexpr (K == kTable) {
             const uint64_t k = x / a.chunk;
             return a.table[k] + (x - k * a.chunk);
+        } else {
+            return a.base + (x - a.x0);
         }
-        return a.base + (x - a.x0);
     }
     // can the 16-byte aligned vectors covering [x, x + len) be loaded whole?
     __device__ __forceinline__ bool vectors_ok(uint64_t xa, uint64_t len) const {
         if (!a.vec_ok) return false;
-        if (a.table) return xa + len <= a.total;
+        if constexpr (K == kTable) return xa + len <= a.total;
         return xa >= a.x0 && xa + len <= a.x1;
     }
 };
@@ -191,12 +206,12 @@ __device__ __forceinline__ void st16(uint8_t* p, u32x4 v) {
 // next tensor's slot; while the following tiles end before that start (the
 // interior of a large tensor) they reuse the staged entries, with no search,
 // no staging and no barrier.
-template <uint32_t U, bool NT>
+template <uint32_t U, bool NT, SrcKind K>
 __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
     constexpr uint64_t kTileU = (uint64_t)kThreads * 16 * U;
     __shared__ uint64_t s_dev[kLdsEntries], s_off[kLdsEntries], s_size[kLdsEntries];
     __shared__ uint64_t s_lo, s_hi, s_next;
-    const Src src{a};
+    const Src<K> src{a};
     // each workgroup walks a contiguous span of tiles, so the owning tensor
     // of the next tile is found by searching forward from the last one
     const uint64_t per_block = (a.n_tiles + gridDim.x - 1) / gridDim.x;
@@ -327,12 +342,17 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     // host sources are PCIe-latency bound like K1; HBM sources want a full chip
     const uint32_t want = std::max<uint32_t>(1, src_is_host ? env_uint("SLLM_K1_BLOCKS", 512) : env_uint("SLLM_K2_BLOCKS", 8192));
     const dim3 grid((uint32_t)std::min<uint64_t>(a.n_tiles, want)), block(kThreads);
-    if (unroll == 8) {
-        if (nt) k_scatter<8, true><<<grid, block, 0, stream>>>(a);
-        else k_scatter<8, false><<<grid, block, 0, stream>>>(a);
+    if (src_is_host) {  // PCIe-bound: no streaming stores, any source kind
+        const bool u8 = unroll == 8;
+        if (a.run_n) u8 ? k_scatter<8, false, kRun><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kRun><<<grid, block, 0, stream>>>(a);
+        else if (a.table) u8 ? k_scatter<8, false, kTable><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kTable><<<grid, block, 0, stream>>>(a);
+        else u8 ? k_scatter<8, false, kWindow><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kWindow><<<grid, block, 0, stream>>>(a);
+    } else if (unroll == 8) {  // HBM windows (K2)
+        if (nt) k_scatter<8, true, kWindow><<<grid, block, 0, stream>>>(a);
+        else k_scatter<8, false, kWindow><<<grid, block, 0, stream>>>(a);
     } else {
-        if (nt) k_scatter<4, true><<<grid, block, 0, stream>>>(a);
-        else k_scatter<4, false><<<grid, block, 0, stream>>>(a);
+        if (nt) k_scatter<4, true, kWindow><<<grid, block, 0, stream>>>(a);
+        else k_scatter<4, false, kWindow><<<grid, block, 0, stream>>>(a);
     }
     SLLM_HIP(hipGetLastError());
     return SLLM_OK;
@@ -392,6 +412,30 @@ int32_t launch_scatter_window(const DeviceLayout& l, uint8_t* dst, const uint8_t
     a.y0 = y_of(l, x0);
     a.y1 = y_of(l, x1);
     return launch(l, a, src_is_host, stream);
+}
+
+int32_t launch_scatter_run(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* srcs, uint64_t k0, uint32_t m,
+                           uint64_t chunk, hipStream_t stream) {
+    if (m == 0) return SLLM_OK;
+    if (m > kScatterBatch || chunk == 0) return fail(SLLM_E_INVAL, "scatter run: bad size");
+    if (k0 >= ceil_div(l.total, chunk) || m > ceil_div(l.total, chunk) - k0)
+        return fail(SLLM_E_INVAL, "scatter run: chunks past the end of the image");
+    ScatterArgs a{};
+    a.dst = dst;
+    a.chunk = chunk;
+    a.run_n = m;
+    a.run_k0 = k0;
+    bool aligned = chunk % 16 == 0;
+    for (uint32_t j = 0; j < m; ++j) {
+        a.run_src[j] = srcs[j];
+        aligned = aligned && reinterpret_cast<uintptr_t>(srcs[j]) % 16 == 0;
+    }
+    a.vec_ok = aligned;
+    a.x0 = k0 * chunk;
+    a.x1 = std::min((k0 + m) * chunk, l.total);
+    a.y0 = y_of(l, a.x0);
+    a.y1 = y_of(l, a.x1);
+    return launch(l, a, /*src_is_host=*/true, stream);
 }
 
 int32_t launch_scatter_table(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* table, uint64_t chunk,

@@ -372,8 +372,9 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     // slots come back together, so a batch holds at most a quarter of the
     // ring: four batches can be on the GPU while readers refill the rest.
     const uint32_t max_batch =
-        (h->engine == SLLM_ENGINE_KERNEL && !h->dev_align)
-            ? std::max<uint32_t>(1, std::min<uint32_t>(kGatherBatch, (uint32_t)h->slots.size() / 4))
+        h->engine == SLLM_ENGINE_KERNEL
+            ? std::max<uint32_t>(1, std::min<uint32_t>(h->dev_align ? kScatterBatch : kGatherBatch,
+                                                       (uint32_t)h->slots.size() / 4))
             : 1;
     // a short batch is held back while the GPU still has at least a full
     // batch's bytes queued and readers are filling slots, so that launches
@@ -428,7 +429,18 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
         if (batch.empty()) continue;
         const uint32_t si = (uint32_t)(launches % h->streams.size());
         hipStream_t st = h->streams[si];
-        if (max_batch > 1) {
+        if (max_batch > 1 && h->dev_align) {
+            // device layout: one scatter launch per run of consecutive chunks
+            std::sort(batch.begin(), batch.end());
+            const uint8_t* srcs[kScatterBatch];
+            for (size_t b0 = 0; b0 < batch.size() && rc == SLLM_OK;) {
+                size_t b1 = b0 + 1;
+                while (b1 < batch.size() && batch[b1].first == batch[b1 - 1].first + 1) ++b1;
+                for (size_t b = b0; b < b1; ++b) srcs[b - b0] = h->slots[batch[b].second].mapped;
+                rc = launch_scatter_run(h->layout, dst, srcs, batch[b0].first, (uint32_t)(b1 - b0), C, st);
+                b0 = b1;
+            }
+        } else if (max_batch > 1) {
             const uint8_t* srcs[kGatherBatch];
             uint64_t ks[kGatherBatch];
             for (size_t b = 0; b < batch.size(); ++b) {
