@@ -371,11 +371,10 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     // batched gather; the other paths move one chunk per call.  A batch's
     // slots come back together, so a batch holds at most a quarter of the
     // ring: four batches can be on the GPU while readers refill the rest.
-    const uint32_t max_batch =
-        h->engine == SLLM_ENGINE_KERNEL
-            ? std::max<uint32_t>(1, std::min<uint32_t>(h->dev_align ? kScatterBatch : kGatherBatch,
-                                                       (uint32_t)h->slots.size() / 4))
-            : 1;
+    const uint32_t quarter = std::max<uint32_t>(1, (uint32_t)h->slots.size() / 4);
+    const uint32_t max_batch = h->engine == SLLM_ENGINE_KERNEL
+                                   ? std::min<uint32_t>(h->dev_align ? kScatterBatch : kGatherBatch, quarter)
+                                   : h->dev_align ? 1 : std::min<uint32_t>(kGatherBatch, quarter);
     // a short batch is held back while the GPU still has at least a full
     // batch's bytes queued and readers are filling slots, so that launches
     // carry about batch_target_bytes() each instead of whatever chunks
@@ -389,7 +388,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     std::vector<std::pair<uint64_t, uint32_t>> batch;
     batch.reserve(max_batch);
     double wait_s = 0;
-    uint64_t moved = 0, launches = 0;
+    uint64_t moved = 0, launches = 0, calls = 0;  // batches; kernel launches and copy calls
     int32_t rc = SLLM_OK;
     while (moved < n && rc == SLLM_OK) {
         rc = reclaim(false);
@@ -438,6 +437,24 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
                 while (b1 < batch.size() && batch[b1].first == batch[b1 - 1].first + 1) ++b1;
                 for (size_t b = b0; b < b1; ++b) srcs[b - b0] = h->slots[batch[b].second].mapped;
                 rc = launch_scatter_run(h->layout, dst, srcs, batch[b0].first, (uint32_t)(b1 - b0), C, st);
+                ++calls;
+                b0 = b1;
+            }
+        } else if (max_batch > 1 && h->engine == SLLM_ENGINE_SDMA) {
+            // copy engines: one copy per run of consecutive chunks whose slots
+            // are adjacent in host memory (slots are handed out in order, so
+            // runs are common)
+            std::sort(batch.begin(), batch.end());
+            for (size_t b0 = 0; b0 < batch.size() && rc == SLLM_OK;) {
+                size_t b1 = b0 + 1;
+                while (b1 < batch.size() && batch[b1].first == batch[b1 - 1].first + 1 &&
+                       h->slots[batch[b1].second].host == h->slots[batch[b1 - 1].second].host + C)
+                    ++b1;
+                const uint64_t x0 = batch[b0].first * C, x1 = std::min(batch[b1 - 1].first * C + C, T);
+                const hipError_t e =
+                    hipMemcpyAsync(dst + x0, h->slots[batch[b0].second].host, x1 - x0, hipMemcpyHostToDevice, st);
+                if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipMemcpyAsync: %s", hipGetErrorString(e));
+                ++calls;
                 b0 = b1;
             }
         } else if (max_batch > 1) {
@@ -448,9 +465,11 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
                 ks[b] = batch[b].first;
             }
             rc = launch_gather_batch(dst, srcs, ks, (uint32_t)batch.size(), C, T, st);
+            ++calls;
         } else {
             const uint64_t k = batch[0].first;
             const Slot& s0 = h->slots[batch[0].second];
+            ++calls;
             rc = move_chunk(h, dst, k, s0.host, s0.mapped, std::min(C, T - k * C), si, st);
         }
         InFlight f;
@@ -463,12 +482,10 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
             f.slots.push_back(item.second);
             f.bytes += std::min(C, T - item.first * C);
         }
-        if (rc == SLLM_OK) {
-            h->inflight.push_back(std::move(f));
-        } else {  // nothing of this batch reached the GPU: its slots are free
-            std::lock_guard<std::mutex> g(mu);
-            for (uint32_t s2 : f.slots) free_q.push_back(s2);
-        }
+        // on error part of the batch may be on the GPU: its slots are not
+        // handed back (the load stops, drains the streams, and the next load
+        // starts from a full free list)
+        if (rc == SLLM_OK) h->inflight.push_back(std::move(f));
         ++launches;
         moved += batch.size();
     }
@@ -484,7 +501,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     h->stats.read_wait_s = wait_s;
     h->stats.bytes_read = bytes_read;
     h->stats.bytes_bounced = bytes_bounced;
-    h->stats.n_launches = launches;
+    h->stats.n_launches = calls;
     h->stats.reader_busy_s = (double)busy_ns.load() * 1e-9;
     h->stats.reader_starved_s = (double)starved_ns.load() * 1e-9;
     if (err != SLLM_OK) {
