@@ -33,7 +33,7 @@ def torch_cuda():
 
 
 def converted(spec):
-    """The workload converted once per box (shared with bench.py)."""
+    """The workload converted once per machine (shared with bench.py)."""
     sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     import bench
 
@@ -208,8 +208,8 @@ def test_llama2_13b_ring_4mib(torch_cuda):
 
 
 def test_llama2_70b_ring_from_shm(torch_cuda):
-    """137.95 GB, 723 tensors (more than the box's free disk, so the file
-    sits in /dev/shm): streamed through a 16 x 64 MiB ring by 16 readers, as
+    """137.95 GB, 723 tensors (larger than the free space of a typical local
+    disk, so the file sits in /dev/shm): streamed through a 16 x 64 MiB ring by 16 readers, as
     the bench runs it; sampled tensors."""
     torch = torch_cuda
     spec = synth.llama2("70b")
