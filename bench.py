@@ -392,7 +392,7 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
             if i:
                 ms.append(e0.elapsed_time(e1))
         k2 = (T + T2) / (statistics.mean(ms) * 1e-3) / 1e9
-        k2c = profiled_counters("k_scatter_repack_llama-2-7b.md", *K2_SOURCES)
+        k2c = profiled_counters("k2_tiles_repack_llama-2-7b.md", *K2_SOURCES)
         out["repack_k2"] = {"dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
                             "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1),
                             "bound": "hbm", "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),

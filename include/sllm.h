@@ -210,7 +210,9 @@ typedef struct sllm_ckpt sllm_ckpt;
  * T = padded sum, file length F) and open dir/sllm.part0.  If `opts->pool`
  * caches this checkpoint, later loads copy from the cached chunks; else they
  * stream the file through ring_slots pool chunks.  opts may be NULL
- * (defaults above, device 0).
+ * (defaults above, device 0).  With a dev_alignment the handle keeps device
+ * tables of 24 bytes per tensor plus 8 bytes per 16 KiB of the device image
+ * (the repack kernel's plan), built here.
  * Errors: INVAL, IO, FORMAT, NOMEM, HIP. */
 int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out);
 

@@ -12,6 +12,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <climits>
 #include <cstdint>
 #include <vector>
 
@@ -26,9 +27,23 @@ struct DeviceLayout {
     uint64_t* d_size = nullptr;     // device: s_i
     uint64_t* d_dev = nullptr;      // device: d_i for i < n, d_n = T2
     std::vector<uint64_t> h_off, h_dev, h_end;  // host: o_i, d_i, o_i + s_i
+    int64_t* d_shift = nullptr;     // device: K2's plan, one entry per kPlanBytes of the device image
+    uint64_t n_shift = 0;           // entries of d_shift: ceil(T2 / kPlanBytes)
     uint8_t* staging = nullptr;     // HBM staging chunks for copy-engine loads
     uint64_t staging_stride = 0;
 };
+
+// K2 from HBM moves the device image in tiles of kTileBytes (kK2Lanes lanes x
+// kK2Vecs 16-byte vectors), one per workgroup.  Its plan holds, for each
+// block of kPlanBytes, the shift o_m - d_m from a destination byte to its
+// partition byte when the block lies inside the data bytes of one tensor m,
+// or kMixedTile when it meets a boundary or padding.
+constexpr uint32_t kK2Lanes = 512;
+constexpr uint32_t kK2Vecs = 1;
+constexpr uint64_t kTileBytes = (uint64_t)kK2Lanes * 16 * kK2Vecs;
+constexpr uint64_t kPlanBytes = 16384;
+static_assert(kPlanBytes % kTileBytes == 0, "a tile lies in one plan block");
+constexpr int64_t kMixedTile = INT64_MIN;
 
 // Upload the tables, compute d on the device and check it against the host
 // plan `dev_off`/`dev_total`; allocate `staging_chunks` HBM chunks of `chunk`

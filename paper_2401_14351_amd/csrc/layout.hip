@@ -4,11 +4,18 @@
 //     tensor index, one workgroup of 16 wave64s: a shuffle scan inside each
 //     wave, the 16 wave totals combined through LDS, a running carry across
 //     blocks of 1024 tensors.
-// K2  index-driven scatter (HBM source) and K1-scatter (mapped pinned host
-//     source): destination-driven.  Each workgroup walks a contiguous span of
-//     16 or 32 KiB tiles of the device image, finds the tensors whose slots
-//     meet a tile (a forward search of d), stages those index entries in LDS
-//     and keeps them for the following tiles they still cover; every lane
+// K2  index-driven scatter from HBM (the repack of a file-layout image, and
+//     copy-engine loads staged in HBM): destination-driven, one 8 KiB tile of
+//     the device image per workgroup of 512 lanes, tiles in dispatch order.
+//     A plan built with the layout gives, per 16 KiB block of the device
+//     image, the shift from a destination byte to its partition byte when the
+//     block lies inside one tensor's data; such tiles copy with one 16-byte
+//     vector per lane after a single table load.  The other tiles take the
+//     general path below.
+// K1-scatter (mapped pinned host source) and K2's general path: each
+//     workgroup walks a span of tiles, finds the tensors whose slots meet a
+//     tile (a forward search of d), stages those index entries in LDS and
+//     keeps them for the following tiles they still cover; every lane
 //     produces aligned 16-byte destination vectors: a straight 16-byte load
 //     when source and destination agree mod 16, two aligned loads and a byte
 //     funnel shift when they do not, zeros for padding.  Only vectors cut by
@@ -200,23 +207,28 @@ __device__ __forceinline__ void st16(uint8_t* p, u32x4 v) {
     }
 }
 
-// One tile: every lane first produces its U destination vectors (all source
+// Index entries of the tensors meeting a tile, staged in LDS.
+struct Staging {
+    uint64_t dev[kLdsEntries], off[kLdsEntries], size[kLdsEntries];
+    uint64_t lo, hi, next;
+};
+
+// Tiles [t_begin, t_end) of the launch, in order (tile t covers destination
+// bytes [(tile0 + t) S, (tile0 + t + 1) S), S = L lanes x 16 B x U).  For
+// each tile every lane first produces its U destination vectors (all source
 // loads in flight together), then stores them.  The index entries of the
 // tensors meeting a tile are staged in LDS together with the start of the
 // next tensor's slot; while the following tiles end before that start (the
 // interior of a large tensor) they reuse the staged entries, with no search,
-// no staging and no barrier.
-template <uint32_t U, bool NT, SrcKind K>
-__global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
-    constexpr uint64_t kTileU = (uint64_t)kThreads * 16 * U;
-    __shared__ uint64_t s_dev[kLdsEntries], s_off[kLdsEntries], s_size[kLdsEntries];
-    __shared__ uint64_t s_lo, s_hi, s_next;
+// no staging and no barrier.  Every lane of the workgroup must call this
+// with the same span (it holds barriers).
+template <uint32_t L, uint32_t U, bool NT, SrcKind K>
+__device__ __forceinline__ void scatter_span(const ScatterArgs& a, Staging& stg, uint64_t t_begin, uint64_t t_end) {
+    constexpr uint64_t kTileU = (uint64_t)L * 16 * U;
+    uint64_t* const s_dev = stg.dev;
+    uint64_t* const s_off = stg.off;
+    uint64_t* const s_size = stg.size;
     const Src<K> src{a};
-    // each workgroup walks a contiguous span of tiles, so the owning tensor
-    // of the next tile is found by searching forward from the last one
-    const uint64_t per_block = (a.n_tiles + gridDim.x - 1) / gridDim.x;
-    const uint64_t t_begin = (uint64_t)blockIdx.x * per_block;
-    const uint64_t t_end = t_begin + per_block < a.n_tiles ? t_begin + per_block : a.n_tiles;
     uint64_t cursor = 0;   // thread 0: owner of the last searched tile's last byte
     bool staged = false;   // LDS holds entries i_lo .. i_lo + cnt - 1 (uniform)
     uint64_t i_lo = 0, cnt = 0, next = 0;  // next: d of the first tensor not staged
@@ -230,28 +242,29 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
                 const uint64_t first =
                     t == t_begin ? owner_global(a.dev, 0, a.n - 1, lo) : owner_from(a.dev, cursor, a.n - 1, lo);
                 cursor = owner_from(a.dev, first, a.n - 1, hi - 1);
-                s_lo = first;
-                s_hi = cursor;
+                stg.lo = first;
+                stg.hi = cursor;
             }
             __syncthreads();
-            i_lo = s_lo;
-            cnt = s_hi - s_lo + 1;
+            i_lo = stg.lo;
+            cnt = stg.hi - stg.lo + 1;
             staged = cnt <= kLdsEntries;
-            if (staged && threadIdx.x < cnt) {
-                s_dev[threadIdx.x] = a.dev[i_lo + threadIdx.x];
-                s_off[threadIdx.x] = a.off[i_lo + threadIdx.x];
-                s_size[threadIdx.x] = a.size[i_lo + threadIdx.x];
-            }
-            if (threadIdx.x == 0) s_next = a.dev[i_lo + cnt];  // d[n] = T2 ends the last slot
+            if (staged)
+                for (uint32_t i = threadIdx.x; i < cnt; i += L) {
+                    s_dev[i] = a.dev[i_lo + i];
+                    s_off[i] = a.off[i_lo + i];
+                    s_size[i] = a.size[i_lo + i];
+                }
+            if (threadIdx.x == 0) stg.next = a.dev[i_lo + cnt];  // d[n] = T2 ends the last slot
             __syncthreads();
-            next = s_next;
+            next = stg.next;
         }
         u32x4 v[U];
         uint32_t whole_mask = 0, in_mask = 0;
 #pragma unroll
         for (uint32_t u = 0; u < U; ++u) {
             v[u] = u32x4{0, 0, 0, 0};
-            const uint64_t y = yt + ((uint64_t)u * kThreads + threadIdx.x) * 16;
+            const uint64_t y = yt + ((uint64_t)u * L + threadIdx.x) * 16;
             if (y + 16 <= lo || y >= hi) continue;
             in_mask |= 1u << u;
             uint64_t dm, om, sm;
@@ -294,7 +307,7 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
 #pragma unroll
         for (uint32_t u = 0; u < U; ++u) {
             if (!(in_mask >> u & 1)) continue;
-            const uint64_t y = yt + ((uint64_t)u * kThreads + threadIdx.x) * 16;
+            const uint64_t y = yt + ((uint64_t)u * L + threadIdx.x) * 16;
             if (whole_mask >> u & 1) {
                 st16<NT>(a.dst + y, v[u]);
             } else {
@@ -302,6 +315,66 @@ __global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
                     if (y + b >= lo && y + b < hi) a.dst[y + b] = (uint8_t)byte_of(v[u], b);
             }
         }
+    }
+}
+
+// K1-scatter (host sources): each workgroup of a persistent grid walks a
+// contiguous span of tiles, so the owner of the next tile is found by
+// searching forward from the last one.
+template <uint32_t U, bool NT, SrcKind K>
+__global__ __launch_bounds__(kThreads) void k_scatter(ScatterArgs a) {
+    __shared__ Staging stg;
+    const uint64_t per_block = (a.n_tiles + gridDim.x - 1) / gridDim.x;
+    const uint64_t t_begin = (uint64_t)blockIdx.x * per_block;
+    const uint64_t t_end = t_begin + per_block < a.n_tiles ? t_begin + per_block : a.n_tiles;
+    scatter_span<kThreads, U, NT, K>(a, stg, t_begin, t_end);
+}
+
+// K2 from HBM: one kTileBytes destination tile per workgroup of kK2Lanes
+// lanes, tiles in dispatch order, so the workgroups in flight sweep a
+// contiguous window of both images (HBM serves that order best).  A tile
+// whose plan block lies inside one tensor's data, and whose source bytes all
+// lie in the window, copies straight from source byte y + shift: one table
+// load, then the data loads.  Every other tile (tensor boundaries, padding,
+// window edges) takes the general path of scatter_span.
+template <bool NT>
+__global__ __launch_bounds__(kK2Lanes) void k2_tiles(ScatterArgs a, const int64_t* __restrict__ shift) {
+    constexpr uint32_t U = kK2Vecs;
+    __shared__ Staging stg;
+    const uint64_t t = a.tile0 + blockIdx.x;
+    const uint64_t yt = t * kTileBytes;
+    const int64_t sh = shift[yt / kPlanBytes];
+    if (sh != kMixedTile && yt >= a.y0 && yt + kTileBytes <= a.y1) {
+        const uint64_t xs = yt + (uint64_t)sh;  // source of the tile's first byte
+        // aligned 16-byte source vectors spanning [xs, xs + S)
+        const uint64_t xa0 = xs & ~15ull, xa1 = (xs + kTileBytes + 15) & ~15ull;
+        if (a.vec_ok && xa0 >= a.x0 && xa1 <= a.x1) {
+            const uint32_t r = (uint32_t)(xs & 15);  // the same for every vector of the tile
+            u32x4 v[U];
+#pragma unroll
+            for (uint32_t u = 0; u < U; ++u) {
+                // partition byte x sits at base + (x - x0); base and x0 are 16-byte aligned
+                const uint8_t* p = a.base + (xs - a.x0) + ((uint64_t)u * kK2Lanes + threadIdx.x) * 16 - r;
+                v[u] = r == 0 ? ld16(p) : funnel(ld16(p), ld16(p + 16), r);
+            }
+#pragma unroll
+            for (uint32_t u = 0; u < U; ++u) st16<NT>(a.dst + yt + ((uint64_t)u * kK2Lanes + threadIdx.x) * 16, v[u]);
+            return;
+        }
+    }
+    scatter_span<kK2Lanes, U, NT, kWindow>(a, stg, blockIdx.x, blockIdx.x + 1);
+}
+
+// K2's plan: shift[p] = o_m - d_m when destination block p (kPlanBytes)
+// lies inside the data bytes of tensor m, else kMixedTile.
+__global__ __launch_bounds__(256) void k3_tile_shift(const uint64_t* __restrict__ dev, const uint64_t* __restrict__ off,
+                                                     const uint64_t* __restrict__ size, uint64_t n, uint64_t n_blocks,
+                                                     int64_t* __restrict__ shift) {
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_blocks; p += stride) {
+        const uint64_t y = p * kPlanBytes;
+        const uint64_t m = owner_global(dev, 0, n - 1, y);  // d_0 = 0 <= y
+        shift[p] = y + kPlanBytes <= dev[m] + size[m] ? (int64_t)(off[m] - dev[m]) : kMixedTile;
     }
 }
 
@@ -324,8 +397,8 @@ uint64_t y_of(const DeviceLayout& l, uint64_t x) {
 }
 
 // Launch shape, read at every launch so that one process can compare shapes:
-// SLLM_K2_UNROLL (4 or 8 vectors per lane), SLLM_K2_NT (streaming stores),
-// SLLM_K2_BLOCKS / SLLM_K1_BLOCKS (grid for HBM / host sources).
+// SLLM_K2_NT (streaming stores for HBM sources), SLLM_K2_UNROLL (4 or 8
+// vectors per lane) and SLLM_K1_BLOCKS (grid) for host sources.
 int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream_t stream) {
     a.off = l.d_off;
     a.size = l.d_size;
@@ -334,26 +407,32 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     a.total = l.total;
     if (a.y0 >= a.y1 || l.n == 0) return SLLM_OK;
     if (a.y1 > l.dev_total) return fail(SLLM_E_INVAL, "scatter: destination range past the image");
+    if (!src_is_host) {  // HBM source (K2): one tile per workgroup, at most 2^31 lanes a launch
+        if (!l.d_shift) return fail(SLLM_E_INVAL, "scatter: the layout has no tile plan");
+        const bool nt = env_uint("SLLM_K2_NT", 1) != 0;
+        const uint64_t t_end = ceil_div(a.y1, kTileBytes);
+        constexpr uint64_t kMaxGrid = (1ull << 31) / kK2Lanes;
+        for (uint64_t t0 = a.y0 / kTileBytes; t0 < t_end; t0 += kMaxGrid) {
+            a.tile0 = t0;
+            a.n_tiles = std::min(kMaxGrid, t_end - t0);
+            const dim3 grid((uint32_t)a.n_tiles);
+            if (nt) k2_tiles<true><<<grid, dim3(kK2Lanes), 0, stream>>>(a, l.d_shift);
+            else k2_tiles<false><<<grid, dim3(kK2Lanes), 0, stream>>>(a, l.d_shift);
+            SLLM_HIP(hipGetLastError());
+        }
+        return SLLM_OK;
+    }
+    // host sources are PCIe-latency bound like K1: a persistent grid of spans
     const uint32_t unroll = env_uint("SLLM_K2_UNROLL", 8) >= 8 ? 8 : 4;
-    const bool nt = env_uint("SLLM_K2_NT", 1) != 0 && !src_is_host;
     const uint64_t tile = (uint64_t)kThreads * 16 * unroll;
     a.tile0 = a.y0 / tile;
     a.n_tiles = ceil_div(a.y1, tile) - a.tile0;
-    // host sources are PCIe-latency bound like K1; HBM sources want a full chip
-    const uint32_t want = std::max<uint32_t>(1, src_is_host ? env_uint("SLLM_K1_BLOCKS", 512) : env_uint("SLLM_K2_BLOCKS", 8192));
+    const uint32_t want = std::max<uint32_t>(1, env_uint("SLLM_K1_BLOCKS", 512));
     const dim3 grid((uint32_t)std::min<uint64_t>(a.n_tiles, want)), block(kThreads);
-    if (src_is_host) {  // PCIe-bound: no streaming stores, any source kind
-        const bool u8 = unroll == 8;
-        if (a.run_n) u8 ? k_scatter<8, false, kRun><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kRun><<<grid, block, 0, stream>>>(a);
-        else if (a.table) u8 ? k_scatter<8, false, kTable><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kTable><<<grid, block, 0, stream>>>(a);
-        else u8 ? k_scatter<8, false, kWindow><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kWindow><<<grid, block, 0, stream>>>(a);
-    } else if (unroll == 8) {  // HBM windows (K2)
-        if (nt) k_scatter<8, true, kWindow><<<grid, block, 0, stream>>>(a);
-        else k_scatter<8, false, kWindow><<<grid, block, 0, stream>>>(a);
-    } else {
-        if (nt) k_scatter<4, true, kWindow><<<grid, block, 0, stream>>>(a);
-        else k_scatter<4, false, kWindow><<<grid, block, 0, stream>>>(a);
-    }
+    const bool u8 = unroll == 8;
+    if (a.run_n) u8 ? k_scatter<8, false, kRun><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kRun><<<grid, block, 0, stream>>>(a);
+    else if (a.table) u8 ? k_scatter<8, false, kTable><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kTable><<<grid, block, 0, stream>>>(a);
+    else u8 ? k_scatter<8, false, kWindow><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kWindow><<<grid, block, 0, stream>>>(a);
     SLLM_HIP(hipGetLastError());
     return SLLM_OK;
 }
@@ -385,6 +464,15 @@ int32_t device_layout_build(const std::vector<uint64_t>& file_off, const std::ve
     SLLM_HIP(hipMemcpy(l.d_size, sizes.data(), bytes, hipMemcpyHostToDevice));
     k3_offsets_scan<<<dim3(1), dim3(1024), 0, nullptr>>>(l.d_size, l.n, dev_align, l.d_dev);
     SLLM_HIP(hipGetLastError());
+    // K2's tile plan, from the scanned offsets (same stream, so in order)
+    l.n_shift = ceil_div(dev_total, kPlanBytes);
+    if (l.n_shift) {
+        SLLM_HIP(hipMalloc(reinterpret_cast<void**>(&l.d_shift), l.n_shift * sizeof(int64_t)));
+        const uint64_t blocks = std::min<uint64_t>(ceil_div(l.n_shift, 256), 4096);
+        k3_tile_shift<<<dim3((uint32_t)blocks), dim3(256), 0, nullptr>>>(l.d_dev, l.d_off, l.d_size, l.n, l.n_shift,
+                                                                         l.d_shift);
+        SLLM_HIP(hipGetLastError());
+    }
     std::vector<uint64_t> got(l.n + 1);
     SLLM_HIP(hipMemcpy(got.data(), l.d_dev, bytes + sizeof(uint64_t), hipMemcpyDeviceToHost));
     for (uint64_t i = 0; i < l.n; ++i)
@@ -396,7 +484,7 @@ int32_t device_layout_build(const std::vector<uint64_t>& file_off, const std::ve
 }
 
 void device_layout_free(DeviceLayout* l) {
-    for (void* p : {(void*)l->d_off, (void*)l->d_size, (void*)l->d_dev, (void*)l->staging})
+    for (void* p : {(void*)l->d_off, (void*)l->d_size, (void*)l->d_dev, (void*)l->d_shift, (void*)l->staging})
         if (p) (void)hipFree(p);
     *l = DeviceLayout{};
 }

@@ -183,7 +183,7 @@ def test_opt125m_file_layout(torch_cuda, opt125m, engine, cached):
 
 
 @pytest.mark.parametrize("engine", ["kernel", "sdma"])
-@pytest.mark.parametrize("shape", [{}, {"SLLM_K2_UNROLL": "4"}, {"SLLM_K2_NT": "1", "SLLM_K2_BLOCKS": "512"},
+@pytest.mark.parametrize("shape", [{}, {"SLLM_K2_UNROLL": "4"}, {"SLLM_K2_NT": "1"},
                                    {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1", "SLLM_K1_BLOCKS": "96"}])
 def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine, shape, monkeypatch):
     """Every launch shape of the scatter and gather kernels gives the same bytes."""
@@ -205,6 +205,61 @@ def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine, shape, mo
         host = dst.cpu().numpy()
         assert (host[len(want2):] == SENTINEL).all()
         assert_same(host[:len(want2)].tobytes(), want2, "repack")
+
+
+@pytest.mark.parametrize("A", [1, 4, 256, 4096])
+def test_repack_tile_paths(torch_cuda, tmp_path, A):
+    """The HBM repack moves 8 KiB destination tiles: tiles inside one
+    tensor's data copy straight (aligned, or shifted when the file layout is
+    not 16-byte aligned), the others (boundaries, padding, zero-size and tiny
+    tensors) take the general path.  Tensors of up to ~200 KB at every file
+    alignment, into A2 = 16 / 256 / 4096, through sllm_repack (the whole
+    image), copy-engine loads from cached chunks (HBM staging windows of
+    merged runs) and streamed ones (one chunk per window; C = 40000 is not a
+    multiple of 16, so every window takes the general path)."""
+    torch = torch_cuda
+    for seed in range(3):
+        spec = synth.tiny(100 + seed, n=48, alignment=A, max_bytes=200_000)
+        tensors = tensors_of(spec)
+        d = str(tmp_path / f"r{seed}")
+        binding.convert(iter(tensors), d, A, 1 << 16)
+        file_img, index = expected(tensors, A)
+        src = torch.frombuffer(bytearray(file_img + bytes(64)), dtype=torch.uint8).to("cuda:0")
+        for A2 in (16, 256, 4096):
+            want, _ = expected(tensors, A, A2)
+            say("repack tiles", A, A2, seed, len(want))
+            with binding.Checkpoint(d, engine="sdma", dev_alignment=A2, chunk_size=1 << 16) as ck:
+                dst = torch.full((len(want) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+                ck.repack(src, dst)
+                torch.cuda.synchronize()
+                host = dst.cpu().numpy()
+                assert (host[len(want):] == SENTINEL).all()
+                assert_same(host[:len(want)].tobytes(), want, f"repack A={A} A2={A2} seed {seed}")
+                assert_same(run_load(torch, ck, len(want)), want, f"streamed sdma C=64K A2={A2}")
+            with binding.Checkpoint(d, engine="sdma", dev_alignment=A2, chunk_size=40000) as ck:
+                assert_same(run_load(torch, ck, len(want)), want, f"streamed sdma C=40000 A2={A2}")
+            with binding.Pool(1 << 16, -(-index.total_bytes // (1 << 16)) + 1) as pool:
+                pool.cache(d)
+                with binding.Checkpoint(d, pool=pool, engine="sdma", dev_alignment=A2) as ck:
+                    assert_same(run_load(torch, ck, len(want)), want, f"cached sdma A2={A2}")
+                pool.evict(d)
+    # 3,000 tensors of 1-32 bytes: at A2 = 16 a tile meets up to 512 slots,
+    # more than the workgroup stages in LDS
+    spec = synth.stress(n=3000, min_bytes=1, max_bytes=32, seed=9)
+    tensors = tensors_of(spec)
+    d = str(tmp_path / "small")
+    binding.convert(iter(tensors), d, A, 1 << 16)
+    file_img, _ = expected(tensors, A)
+    want, _ = expected(tensors, A, 16)
+    src = torch.frombuffer(bytearray(file_img + bytes(64)), dtype=torch.uint8).to("cuda:0")
+    with binding.Checkpoint(d, engine="sdma", dev_alignment=16, chunk_size=1 << 16) as ck:
+        dst = torch.full((len(want) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+        ck.repack(src, dst)
+        torch.cuda.synchronize()
+        host = dst.cpu().numpy()
+        assert (host[len(want):] == SENTINEL).all()
+        assert_same(host[:len(want)].tobytes(), want, f"repack of 3,000 small tensors, A={A}")
+        assert_same(run_load(torch, ck, len(want)), want, f"streamed sdma, 3,000 small tensors, A={A}")
 
 
 def test_stress_prefix_device_layout(torch_cuda, tmp_path):
