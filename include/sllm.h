@@ -224,8 +224,10 @@ uint64_t sllm_total_bytes(const sllm_ckpt* h);
  * included (as zero); bytes past it are untouched.  Returns once every file
  * read has finished and every copy or kernel has been enqueued; completion is
  * ordered on `stream`: work queued there after this call sees every byte.
- * Errors: INVAL, RANGE (dst_bytes < total), IO, HIP, BUSY (another load on
- * this handle).  On error, in-flight work is drained and the destination's
+ * Errors: INVAL (dev_dst is not device memory of the handle's device, or
+ * not 16-byte aligned), RANGE (dst_bytes < total, or the range runs past the
+ * end of dev_dst's allocation), IO, HIP, BUSY (another load on this
+ * handle).  On error, in-flight work is drained and the destination's
  * contents are unspecified; the handle stays usable. */
 int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream);
 
@@ -234,7 +236,8 @@ int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream)
  * dev_alignment = 0) and dst receives T2 bytes laid out with the handle's
  * dev_alignment.  src and dst are device pointers, 16-byte aligned, and must
  * not overlap.  Enqueued on `stream`.
- * Errors: INVAL (handle opened without dev_alignment, overlap), RANGE, HIP. */
+ * Errors: INVAL (handle opened without dev_alignment, overlap, a buffer that
+ * is not device memory of the handle's device), RANGE, HIP. */
 int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes,
                     void* dst_dev, uint64_t dst_bytes, void* stream);
 

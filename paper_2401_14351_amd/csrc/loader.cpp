@@ -136,6 +136,33 @@ int32_t join_streams(sllm_ckpt* h, hipStream_t user) {
     return SLLM_OK;
 }
 
+// [p, p + bytes) must be device memory of `device` inside one allocation: a
+// kernel or copy that wrote to a host address or past an allocation would
+// fault the GPU instead of failing the call.
+int32_t check_device_range(const void* p, uint64_t bytes, int device, const char* what) {
+    if (!bytes) return SLLM_OK;
+    hipPointerAttribute_t at{};
+    if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();  // leave no error behind for later launch checks
+        return fail(SLLM_E_INVAL, "%s %p is not device memory", what, p);
+    }
+    if (at.type != hipMemoryTypeDevice && at.type != hipMemoryTypeManaged)
+        return fail(SLLM_E_INVAL, "%s %p is not device memory", what, p);
+    if (at.type == hipMemoryTypeDevice && at.device != device)
+        return fail(SLLM_E_INVAL, "%s is memory of device %d, not of the handle's device %d", what, at.device, device);
+    void* base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess || !base) {
+        (void)hipGetLastError();  // no range known (e.g. managed memory): nothing more to check
+        return SLLM_OK;
+    }
+    const uint64_t off = (uint64_t)(static_cast<const uint8_t*>(p) - static_cast<const uint8_t*>(base));
+    if (off + bytes > size)
+        return fail(SLLM_E_RANGE, "%s: %llu bytes from %p run past the end of its allocation", what,
+                    (unsigned long long)bytes, p);
+    return SLLM_OK;
+}
+
 uint64_t sdma_max_copy() {
     static const uint64_t v = [] {
         const char* s = std::getenv("SLLM_SDMA_MAX_COPY_MB");
@@ -690,6 +717,7 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
                     (unsigned long long)h->dev_total);
     DeviceGuard guard(h->device);
     if (!guard.ok()) return fail(SLLM_E_HIP, "cannot make device %d current", h->device);
+    SLLM_TRY(check_device_range(dev_dst, h->dev_total, h->device, "destination"));
     hipStream_t user = static_cast<hipStream_t>(stream);
     const double t0 = now_s();
     h->stats.bytes_loaded = 0;
@@ -737,6 +765,8 @@ extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t
     if (!h->dev_total) return SLLM_OK;
     DeviceGuard guard(h->device);
     if (!guard.ok()) return fail(SLLM_E_HIP, "cannot make device %d current", h->device);
+    SLLM_TRY(check_device_range(src_dev, h->ix.total, h->device, "source"));
+    SLLM_TRY(check_device_range(dst_dev, h->dev_total, h->device, "destination"));
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t* dst = static_cast<uint8_t*>(dst_dev);
     return launch_scatter_window(h->layout, dst, static_cast<const uint8_t*>(src_dev), 0, h->ix.total,

@@ -79,11 +79,25 @@ def test_llama2_7b_cached_k1(torch_cuda):
             ck.load_into(buf, s)
             s.synchronize()
             assert ck.stats()["n_launches"] == 1
+        # the HBM repack the bench times: A2 = 4 KiB, one K2 launch over the image
+        sizes = [t.nbytes for t in spec.tensors]
+        d2, T2 = oracle.plan_layout(sizes, 4096)
+        with binding.Checkpoint(d, pool=pool, dev_alignment=4096) as ck:
+            assert ck.total_bytes == T2 and [t.offset for t in ck.tensors()] == d2
+            out = torch.full((T2 + 4096,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+            ck.repack(buf, out, s)
+            s.synchronize()
         pool.evict(d)
     assert bool((buf[T:] == SENTINEL).all())
-    check_zero_gaps(torch, buf, offsets, [t.nbytes for t in spec.tensors], T)
+    check_zero_gaps(torch, buf, offsets, sizes, T)
     check_tensors(torch, spec, buf, offsets)
     say("7b: all tensors match")
+    # every tensor of this model is a multiple of 4 KiB, so the 4 KiB layout
+    # is the file layout: the repacked image equals the verified load
+    assert d2 == offsets and T2 == T
+    assert bool((out[T2:] == SENTINEL).all())
+    assert torch.equal(out[:T2], buf[:T])
+    say("7b: HBM repack matches")
 
 
 def test_stress_8g_file_and_device_layout(torch_cuda):

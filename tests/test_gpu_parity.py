@@ -321,6 +321,15 @@ def test_load_errors(torch_cuda, opt125m):
         with pytest.raises(binding.SllmError) as ei:
             ck.find("no.such.tensor")
         assert ei.value.code == -8
+        # host memory (pageable or pinned) is refused before any device work
+        host = np.zeros(ck.total_bytes + 16, np.uint8)
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load((host.ctypes.data + 15) & ~15, ck.total_bytes)
+        assert ei.value.code == -1 and "not device memory" in ei.value.message
+        pinned = torch.empty(ck.total_bytes, dtype=torch.uint8, pin_memory=True)
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load_into(pinned)
+        assert ei.value.code == -1 and "not device memory" in ei.value.message
         # the handle still works after the errors
         want, _ = expected(tensors, spec.alignment)
         assert_same(run_load(torch, ck, len(want)), want, "after errors")
