@@ -138,7 +138,33 @@ def host_info():
     except OSError:
         nodes = []
     return {"nproc": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(), "cpu_model": model,
-            "numa_nodes": len(nodes) or None}
+            "numa_nodes": len(nodes) or None, "gpu_links": gpu_links()}
+
+
+def gpu_links():
+    """PCIe link (speed, width) of each AMD GPU, from sysfs: the host link
+    that bounds every DRAM -> HBM transfer."""
+    out = []
+    base = "/sys/class/drm"
+    try:
+        cards = sorted(c for c in os.listdir(base) if c.startswith("card") and c[4:].isdigit())
+    except OSError:
+        return out
+    for c in cards:
+        dev = os.path.join(base, c, "device")
+
+        def read(name):
+            try:
+                return open(os.path.join(dev, name)).read().strip()
+            except OSError:
+                return None
+
+        if read("vendor") != "0x1002":
+            continue
+        out.append({"pci": os.path.basename(os.path.realpath(dev)), "speed": read("current_link_speed"),
+                    "width": read("current_link_width"), "max_speed": read("max_link_speed"),
+                    "max_width": read("max_link_width")})
+    return out
 
 
 def cpu_baseline(d: str, budget_s: float):
@@ -622,7 +648,8 @@ def main():
                      "kernel_ms": round(statistics.mean(kernel_ms), 3),
                      "peak_measured": None if h2d_peak is None else round(h2d_peak, 3),
                      "frac_measured": None if h2d_peak is None else round(achieved / h2d_peak, 4),
-                     "hbm_copy_measured": None if hbm_peak is None else round(hbm_peak, 1)},
+                     "hbm_copy_measured": None if hbm_peak is None else round(hbm_peak, 1),
+                     "link": next((f"{g['speed']} x{g['width']}" for g in gpu_links()), None)},
         "cpu_baseline": cpu,
         "extras": extras,
     }
