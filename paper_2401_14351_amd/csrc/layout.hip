@@ -397,8 +397,9 @@ uint64_t y_of(const DeviceLayout& l, uint64_t x) {
 }
 
 // Launch shape, read at every launch so that one process can compare shapes:
-// SLLM_K2_NT (streaming stores for HBM sources), SLLM_K2_UNROLL (4 or 8
-// vectors per lane) and SLLM_K1_BLOCKS (grid) for host sources.
+// SLLM_K2_NT (streaming stores) and SLLM_K2_MAX_GRID (workgroups a launch)
+// for HBM sources; SLLM_K2_UNROLL (4 or 8 vectors per lane) and
+// SLLM_K1_BLOCKS (grid) for host sources.
 int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream_t stream) {
     a.off = l.d_off;
     a.size = l.d_size;
@@ -407,14 +408,17 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     a.total = l.total;
     if (a.y0 >= a.y1 || l.n == 0) return SLLM_OK;
     if (a.y1 > l.dev_total) return fail(SLLM_E_INVAL, "scatter: destination range past the image");
-    if (!src_is_host) {  // HBM source (K2): one tile per workgroup, at most 2^31 lanes a launch
+    if (!src_is_host) {  // HBM source (K2): one tile per workgroup
         if (!l.d_shift) return fail(SLLM_E_INVAL, "scatter: the layout has no tile plan");
         const bool nt = env_uint("SLLM_K2_NT", 1) != 0;
         const uint64_t t_end = ceil_div(a.y1, kTileBytes);
+        // at most 2^31 lanes a launch (SLLM_K2_MAX_GRID lowers it, to exercise
+        // the split on small images)
         constexpr uint64_t kMaxGrid = (1ull << 31) / kK2Lanes;
-        for (uint64_t t0 = a.y0 / kTileBytes; t0 < t_end; t0 += kMaxGrid) {
+        const uint64_t max_grid = std::max<uint64_t>(1, std::min<uint64_t>(kMaxGrid, env_uint("SLLM_K2_MAX_GRID", kMaxGrid)));
+        for (uint64_t t0 = a.y0 / kTileBytes; t0 < t_end; t0 += max_grid) {
             a.tile0 = t0;
-            a.n_tiles = std::min(kMaxGrid, t_end - t0);
+            a.n_tiles = std::min(max_grid, t_end - t0);
             const dim3 grid((uint32_t)a.n_tiles);
             if (nt) k2_tiles<true><<<grid, dim3(kK2Lanes), 0, stream>>>(a, l.d_shift);
             else k2_tiles<false><<<grid, dim3(kK2Lanes), 0, stream>>>(a, l.d_shift);

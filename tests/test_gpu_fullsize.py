@@ -256,12 +256,13 @@ def test_llama2_70b_ring_from_shm(torch_cuda):
 def test_stress_full_ring_from_shm(torch_cuda):
     """The full stress workload (20,000 tensors, all four dtypes, sizes
     log-uniform over [256 B, 64 MiB], 4 KiB alignment, 1 MiB chunks: about
-    108 GB, in /dev/shm) streamed through a 1 GiB ring; sampled tensors and
-    the padding after them."""
+    108 GB, in /dev/shm) streamed through a 1 GiB ring, then repacked in HBM
+    into A2 = 256; sampled tensors and the padding after them, in both
+    images."""
     torch = torch_cuda
     spec = synth.config("stress")
     d = shm_dir(spec.name)
-    buf = None
+    buf = out = None
     try:
         converted_at(spec, d)
         sizes = [t.nbytes for t in spec.tensors]
@@ -278,9 +279,24 @@ def test_stress_full_ring_from_shm(torch_cuda):
         check_sampled_gaps(torch, buf, offsets, sizes, T, idx)
         check_tensors(torch, spec, buf, offsets, indices=idx)
         say("stress: sampled tensors match")
+        # the HBM repack of the whole image into A2 = 256 (about 13 million
+        # tiles, several K2 launches); sampled tensors at their device offsets
+        d2, T2 = oracle.plan_layout(sizes, 256)
+        with binding.Checkpoint(d, dev_alignment=256) as ck:
+            assert ck.total_bytes == T2 and [t.offset for t in ck.tensors()] == d2
+            out = torch.full((T2 + 4096,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+            ck.repack(buf, out)
+            torch.cuda.synchronize()
+        buf = None
+        torch.cuda.empty_cache()
+        assert bool((out[T2:] == SENTINEL).all())
+        check_sampled_gaps(torch, out, d2, sizes, T2, idx)
+        check_tensors(torch, spec, out, d2, indices=idx)
+        out = None
+        say("stress: repacked sampled tensors match")
     finally:
         import shutil
 
         shutil.rmtree(d, ignore_errors=True)
-        buf = None  # drop the image before handing its memory back
+        buf = out = None  # drop the images before handing their memory back
         torch.cuda.empty_cache()

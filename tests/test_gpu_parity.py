@@ -183,7 +183,7 @@ def test_opt125m_file_layout(torch_cuda, opt125m, engine, cached):
 
 
 @pytest.mark.parametrize("engine", ["kernel", "sdma"])
-@pytest.mark.parametrize("shape", [{}, {"SLLM_K2_UNROLL": "4"}, {"SLLM_K2_NT": "1"},
+@pytest.mark.parametrize("shape", [{}, {"SLLM_K2_UNROLL": "4"}, {"SLLM_K2_NT": "0", "SLLM_K2_MAX_GRID": "997"},
                                    {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1", "SLLM_K1_BLOCKS": "96"}])
 def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine, shape, monkeypatch):
     """Every launch shape of the scatter and gather kernels gives the same bytes."""
