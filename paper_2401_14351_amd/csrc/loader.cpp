@@ -163,13 +163,12 @@ int32_t check_device_range(const void* p, uint64_t bytes, int device, const char
     return SLLM_OK;
 }
 
+// Largest merged copy of a cached partition (SLLM_SDMA_MAX_COPY_MB, default
+// 256), read at every load so that one process can compare sizes.
 uint64_t sdma_max_copy() {
-    static const uint64_t v = [] {
-        const char* s = std::getenv("SLLM_SDMA_MAX_COPY_MB");
-        long mb = s ? std::strtol(s, nullptr, 10) : 0;
-        return (mb > 0 ? (uint64_t)mb : 256ull) << 20;
-    }();
-    return v;
+    const char* s = std::getenv("SLLM_SDMA_MAX_COPY_MB");
+    const long mb = s ? std::strtol(s, nullptr, 10) : 0;
+    return (mb > 0 ? (uint64_t)mb : 256ull) << 20;
 }
 
 // Move one chunk (partition bytes [x0, x0 + len)) from a pinned slot to the
