@@ -4,25 +4,23 @@
 // Two sources feed a load:
 //  * cached: the partition already sits in pool chunks (the DRAM tier); the
 //    whole image moves in one K1 launch or in merged SDMA copies.
-//  * streamed: a task-queue pipeline.  I/O threads take the next chunk
-//    number, read that chunk from the file into a free pinned slot and queue
-//    (chunk, slot) for the issue loop, which moves it to the GPU on one of
-//    the copy streams and records the slot's completion event.  A slot is
-//    refilled only after its event has fired.
+//  * streamed: the task-queue pipeline of pipeline.cpp.  I/O threads take
+//    the next chunk number, read that chunk from the file into a free pinned
+//    slot and queue (chunk, slot); the issue loop moves ready chunks to the
+//    GPU in batches (GpuSink below: one batch per copy stream in turn, then
+//    one event).  A slot is refilled only after its batch's event has fired.
 #include <algorithm>
 #include <atomic>
-#include <chrono>
-#include <condition_variable>
 #include <cstdlib>
 #include <cstring>
 #include <deque>
 #include <mutex>
-#include <thread>
 #include <unordered_map>
 
 #include "device_layout.hpp"
 #include "hip_util.hpp"
 #include "kernels.hpp"
+#include "pipeline.hpp"
 #include "pool.hpp"
 
 using namespace sllm;
@@ -34,13 +32,6 @@ struct Slot {
     uint8_t* host = nullptr;
     const uint8_t* mapped = nullptr;  // device-visible address of the same bytes
     hipEvent_t done = nullptr;        // the event of a batch this slot heads
-};
-
-// A batch of slots the GPU may still read, and the event that ends it.
-struct InFlight {
-    hipEvent_t ev = nullptr;
-    std::vector<uint32_t> slots;
-    uint64_t bytes = 0;  // partition bytes the batch moves
 };
 
 }  // namespace
@@ -61,7 +52,8 @@ struct sllm_ckpt {
     uint32_t io_threads = 4, n_streams = 2, ring_slots = 8, engine = SLLM_ENGINE_KERNEL, flags = 0;
     std::vector<Slot> slots;
     std::vector<uint32_t> slot_ids;
-    std::deque<InFlight> inflight;  // batches of the last streamed load not yet seen done
+    std::deque<InFlightBatch> inflight;  // batches of the last streamed load not yet seen done
+                                         // (token = the slot whose event ends the batch)
     std::vector<hipStream_t> streams;
     std::vector<hipEvent_t> join_ev;
     hipEvent_t fork_ev = nullptr, t0_ev = nullptr, t1_ev = nullptr;
@@ -82,7 +74,7 @@ void release(sllm_ckpt* h) {
         DeviceGuard guard(h->device);
         for (hipStream_t s : h->streams)
             if (s) (void)hipStreamSynchronize(s);
-        for (const InFlight& b : h->inflight) (void)hipEventSynchronize(b.ev);
+        for (const InFlightBatch& b : h->inflight) (void)hipEventSynchronize(h->slots[b.token].done);
         for (Slot& s : h->slots)
             if (s.done) (void)hipEventDestroy(s.done);
         for (hipEvent_t e : h->join_ev)
@@ -245,14 +237,6 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     return join_streams(h, user);
 }
 
-// The streamed pipeline: io_threads readers feed the issue loop through two
-// queues.  Readers only read: they take a free slot, fill it with the next
-// chunk and queue it.  The issue loop owns every device call: it moves each
-// pass's ready chunks (one batched gather, or one copy / scatter), records
-// one event per batch, and returns a batch's slots to the free queue once
-// that event has completed, polling in-flight batches in order and blocking
-// on the oldest only when every slot is on the GPU.  Batches still in flight
-// when the load returns are reclaimed at the start of the next one.
 // Bytes a streamed gather batch waits to collect (SLLM_BATCH_TARGET_MB,
 // default 64; 0 launches whatever is ready).
 uint64_t batch_target_bytes() {
@@ -262,12 +246,6 @@ uint64_t batch_target_bytes() {
     char* end = nullptr;
     const long v = std::strtol(s, &end, 10);
     return (end && *end == '\0' && v >= 0) ? (uint64_t)v << 20 : kDefault;
-}
-
-int32_t reclaim_all(sllm_ckpt* h) {
-    for (const InFlight& b : h->inflight) SLLM_HIP(hipEventSynchronize(b.ev));
-    h->inflight.clear();
-    return SLLM_OK;
 }
 
 // After a successful streamed load with kept slots, hand them to the pool as
@@ -287,254 +265,121 @@ void adopt_kept(sllm_ckpt* h) {
     h->keep = false;
 }
 
-int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
-    const uint64_t C = h->chunk, T = h->ix.total;
-    const uint64_t n = ceil_div(T, C);
-    const uint64_t read_end = h->file.direct ? h->ix.file_bytes : T;
-    h->stats.n_chunks = n;
-    SLLM_TRY(reclaim_all(h));
-    SLLM_TRY(ensure_streams(h));
-    SLLM_TRY(fork_streams(h, user));
+// The GPU side of a streamed load.  Batch `seq` goes to copy stream
+// seq mod S: the kernel engine moves the batch in one batched gather (file
+// layout) or one K1-scatter launch per run of consecutive chunks (device
+// layout); the copy engines take one copy per run of consecutive chunks
+// whose slots are adjacent in host memory (slots are handed out in order, so
+// runs are common), or, with a device layout, one chunk per batch through
+// the stream's HBM staging chunk and K2.  The event of the batch's first
+// slot, recorded after its work on the same stream, ends the batch.
+class GpuSink final : public BatchSink {
+  public:
+    GpuSink(sllm_ckpt* h, uint8_t* dst, uint32_t max_batch) : h_(h), dst_(dst), max_batch_(max_batch) {}
 
-    std::mutex mu;
-    std::condition_variable cv_free, cv_ready;
-    std::deque<uint32_t> free_q;
-    std::deque<std::pair<uint64_t, uint32_t>> ready_q;
-    if (!h->keep)
-        for (uint32_t i = 0; i < h->slots.size(); ++i) free_q.push_back(i);
-    std::atomic<uint64_t> next{0};
-    uint32_t reading = 0;  // slots held by readers
-    bool stop = false;
-    int32_t err = SLLM_OK;
-    std::string err_msg;
-    uint64_t bytes_read = 0, bytes_bounced = 0;
-    std::atomic<uint64_t> busy_ns{0}, starved_ns{0};
-
-    auto set_error = [&](int32_t st) {  // caller holds mu
-        if (err == SLLM_OK) {
-            err = st;
-            err_msg = sllm_last_error();
-        }
-        stop = true;
-        cv_free.notify_all();
-        cv_ready.notify_all();
-    };
-
-    auto reader = [&] {
-        for (;;) {
-            const uint64_t k = next.fetch_add(1);
-            if (k >= n) return;
-            uint32_t si;
-            {
-                const double w0 = now_s();
-                std::unique_lock<std::mutex> lk(mu);
-                if (h->keep) {  // chunk k has a slot of its own
-                    if (stop) return;
-                    si = (uint32_t)k;
-                } else {
-                    cv_free.wait(lk, [&] { return stop || !free_q.empty(); });
-                    starved_ns += (uint64_t)((now_s() - w0) * 1e9);
-                    if (stop) return;
-                    si = free_q.front();
-                    free_q.pop_front();
-                }
-                ++reading;
+    int32_t move(const ChunkSlot* b, uint32_t n, uint64_t seq, uint64_t* token) override {
+        const uint64_t C = h_->chunk, T = h_->ix.total;
+        const uint32_t si = (uint32_t)(seq % h_->streams.size());
+        hipStream_t st = h_->streams[si];
+        if (max_batch_ > 1 && h_->dev_align) {
+            const uint8_t* srcs[kScatterBatch];
+            for (uint32_t b0 = 0; b0 < n;) {
+                uint32_t b1 = b0 + 1;
+                while (b1 < n && b[b1].chunk == b[b1 - 1].chunk + 1) ++b1;
+                for (uint32_t j = b0; j < b1; ++j) srcs[j - b0] = h_->slots[b[j].slot].mapped;
+                ++calls;
+                SLLM_TRY(launch_scatter_run(h_->layout, dst_, srcs, b[b0].chunk, b1 - b0, C, st));
+                b0 = b1;
             }
-            const uint64_t off = k * C, len = std::min(C, read_end - off);
-            uint64_t bounced = 0;
-            const double r0 = now_s();
-            const int32_t st = read_chunk(h->file, h->slots[si].host, len, off, h->data_path, &bounced);
-            busy_ns += (uint64_t)((now_s() - r0) * 1e9);
-            std::lock_guard<std::mutex> g(mu);
-            --reading;
-            if (st != SLLM_OK) {
-                if (!h->keep) free_q.push_back(si);
-                set_error(st);
-                return;
+        } else if (max_batch_ > 1 && h_->engine == SLLM_ENGINE_SDMA) {
+            for (uint32_t b0 = 0; b0 < n;) {
+                uint32_t b1 = b0 + 1;
+                while (b1 < n && b[b1].chunk == b[b1 - 1].chunk + 1 &&
+                       h_->slots[b[b1].slot].host == h_->slots[b[b1 - 1].slot].host + C)
+                    ++b1;
+                const uint64_t x0 = b[b0].chunk * C, x1 = std::min(b[b1 - 1].chunk * C + C, T);
+                ++calls;
+                SLLM_HIP(hipMemcpyAsync(dst_ + x0, h_->slots[b[b0].slot].host, x1 - x0, hipMemcpyHostToDevice, st));
+                b0 = b1;
             }
-            bytes_read += len;
-            bytes_bounced += bounced;
-            ready_q.emplace_back(k, si);
-            cv_ready.notify_one();
+        } else if (max_batch_ > 1) {
+            const uint8_t* srcs[kGatherBatch];
+            uint64_t ks[kGatherBatch];
+            for (uint32_t j = 0; j < n; ++j) {
+                srcs[j] = h_->slots[b[j].slot].mapped;
+                ks[j] = b[j].chunk;
+            }
+            ++calls;
+            SLLM_TRY(launch_gather_batch(dst_, srcs, ks, n, C, T, st));
+        } else {
+            const Slot& s0 = h_->slots[b[0].slot];
+            ++calls;
+            SLLM_TRY(move_chunk(h_, dst_, b[0].chunk, s0.host, s0.mapped, std::min(C, T - b[0].chunk * C), si, st));
         }
-    };
-
-    const uint32_t nt = (uint32_t)std::min<uint64_t>(h->io_threads, n);
-    std::vector<std::thread> threads;
-    try {
-        threads.reserve(nt);
-        for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader);
-    } catch (...) {  // could not start every reader: stop the ones that run
-        {
-            std::lock_guard<std::mutex> g(mu);
-            stop = true;
-            cv_free.notify_all();
-        }
-        for (auto& t : threads) t.join();
-        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
-        return fail(SLLM_E_NOMEM, "cannot start %u I/O threads", nt);
+        SLLM_HIP(hipEventRecord(h_->slots[b[0].slot].done, st));
+        *token = b[0].slot;
+        return SLLM_OK;
     }
 
-    // give the slots of completed batches back to the readers; with `block`,
-    // wait for the oldest batch first
-    auto reclaim = [&](bool block) -> int32_t {
-        while (!h->inflight.empty()) {
-            hipError_t e = block ? hipEventSynchronize(h->inflight.front().ev) : hipEventQuery(h->inflight.front().ev);
-            block = false;
-            if (e == hipErrorNotReady) break;
-            if (e != hipSuccess) return fail(SLLM_E_HIP, "waiting for a batch: %s", hipGetErrorString(e));
-            if (!h->keep) {  // kept slots are not refilled
-                std::lock_guard<std::mutex> g(mu);
-                for (uint32_t si : h->inflight.front().slots) free_q.push_back(si);
-            }
-            cv_free.notify_all();
-            h->inflight.pop_front();
-        }
-        return SLLM_OK;
-    };
+    int32_t done(uint64_t token, bool block) override {
+        hipEvent_t ev = h_->slots[token].done;
+        const hipError_t e = block ? hipEventSynchronize(ev) : hipEventQuery(ev);
+        if (e == hipErrorNotReady) return 0;
+        if (e != hipSuccess) return fail(SLLM_E_HIP, "waiting for a batch: %s", hipGetErrorString(e));
+        return 1;
+    }
 
+    void drain() override {
+        for (hipStream_t s : h_->streams) (void)hipStreamSynchronize(s);
+    }
+
+    uint64_t calls = 0;  // kernel launches and copy calls
+
+  private:
+    sllm_ckpt* h_;
+    uint8_t* dst_;
+    uint32_t max_batch_;
+};
+
+int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
+    const uint64_t C = h->chunk, T = h->ix.total;
+    h->stats.n_chunks = ceil_div(T, C);
+    SLLM_TRY(ensure_streams(h));
     // kernel loads in the file layout move every chunk that is ready in one
-    // batched gather; the other paths move one chunk per call.  A batch's
-    // slots come back together, so a batch holds at most a quarter of the
-    // ring: four batches can be on the GPU while readers refill the rest.
+    // batched gather, device layouts one scatter per run of consecutive
+    // chunks, the copy engines one copy per run of adjacent slots (one chunk
+    // per batch with a device layout).  A batch's slots come back together,
+    // so a batch holds at most a quarter of the ring: four batches can be on
+    // the GPU while readers refill the rest.
     const uint32_t quarter = std::max<uint32_t>(1, (uint32_t)h->slots.size() / 4);
     const uint32_t max_batch = h->engine == SLLM_ENGINE_KERNEL
                                    ? std::min<uint32_t>(h->dev_align ? kScatterBatch : kGatherBatch, quarter)
                                    : h->dev_align ? 1 : std::min<uint32_t>(kGatherBatch, quarter);
-    // a short batch is held back while the GPU still has at least a full
-    // batch's bytes queued and readers are filling slots, so that launches
-    // carry about batch_target_bytes() each instead of whatever chunks
-    // arrived last (a gather launch ramps up and drains at its ends)
-    const uint64_t target = std::min<uint64_t>(max_batch, std::max<uint64_t>(1, batch_target_bytes() / C));
-    auto queued_bytes = [&] {
-        uint64_t b = 0;
-        for (const InFlight& f : h->inflight) b += f.bytes;
-        return b;
+    GpuSink sink(h, dst, max_batch);
+    SLLM_TRY(reclaim_batches(sink, h->inflight));
+    SLLM_TRY(fork_streams(h, user));
+
+    StreamPlan plan;
+    plan.chunk = C;
+    plan.total = T;
+    plan.read_end = h->file.direct ? h->ix.file_bytes : T;
+    plan.io_threads = h->io_threads;
+    plan.n_slots = (uint32_t)h->slots.size();
+    plan.max_batch = max_batch;
+    plan.target = std::max<uint64_t>(1, batch_target_bytes() / C);
+    plan.keep = h->keep;
+    auto read = [h](uint64_t k, uint32_t si, uint64_t len, uint64_t* bounced) {
+        return read_chunk(h->file, h->slots[si].host, len, k * h->chunk, h->data_path, bounced);
     };
-    std::vector<std::pair<uint64_t, uint32_t>> batch;
-    batch.reserve(max_batch);
-    double wait_s = 0;
-    uint64_t moved = 0, launches = 0, calls = 0;  // batches; kernel launches and copy calls
-    int32_t rc = SLLM_OK;
-    while (moved < n && rc == SLLM_OK) {
-        rc = reclaim(false);
-        if (rc != SLLM_OK) break;
-        batch.clear();
-        bool wait_gpu = false;
-        {
-            const double w0 = now_s();
-            std::unique_lock<std::mutex> lk(mu);
-            // readers are reading, or will start on a free slot (a chunk of
-            // their own when slots are kept)
-            const bool readers_busy = reading > 0 || (h->keep ? next.load() < n : !free_q.empty());
-            if (ready_q.empty() && !stop) {
-                if (!readers_busy && !h->inflight.empty())
-                    wait_gpu = true;  // every slot is on the GPU
-                else
-                    cv_ready.wait_for(lk, std::chrono::microseconds(200), [&] { return stop || !ready_q.empty(); });
-            }
-            const uint64_t fill = std::min<uint64_t>(target, n - moved);
-            bool hold = false;
-            if (!wait_gpu && !stop && ready_q.size() < fill && readers_busy && queued_bytes() >= target * C) {
-                cv_ready.wait_for(lk, std::chrono::microseconds(50),
-                                  [&] { return stop || ready_q.size() >= fill; });
-                hold = !stop && ready_q.size() < fill;  // still short: reclaim, then look again
-            }
-            wait_s += now_s() - w0;
-            if (stop && ready_q.empty()) break;  // a reader failed
-            while (!hold && !ready_q.empty() && batch.size() < max_batch) {
-                batch.push_back(ready_q.front());
-                ready_q.pop_front();
-            }
-        }
-        if (wait_gpu) {
-            rc = reclaim(true);
-            continue;
-        }
-        if (batch.empty()) continue;
-        const uint32_t si = (uint32_t)(launches % h->streams.size());
-        hipStream_t st = h->streams[si];
-        if (max_batch > 1 && h->dev_align) {
-            // device layout: one scatter launch per run of consecutive chunks
-            std::sort(batch.begin(), batch.end());
-            const uint8_t* srcs[kScatterBatch];
-            for (size_t b0 = 0; b0 < batch.size() && rc == SLLM_OK;) {
-                size_t b1 = b0 + 1;
-                while (b1 < batch.size() && batch[b1].first == batch[b1 - 1].first + 1) ++b1;
-                for (size_t b = b0; b < b1; ++b) srcs[b - b0] = h->slots[batch[b].second].mapped;
-                rc = launch_scatter_run(h->layout, dst, srcs, batch[b0].first, (uint32_t)(b1 - b0), C, st);
-                ++calls;
-                b0 = b1;
-            }
-        } else if (max_batch > 1 && h->engine == SLLM_ENGINE_SDMA) {
-            // copy engines: one copy per run of consecutive chunks whose slots
-            // are adjacent in host memory (slots are handed out in order, so
-            // runs are common)
-            std::sort(batch.begin(), batch.end());
-            for (size_t b0 = 0; b0 < batch.size() && rc == SLLM_OK;) {
-                size_t b1 = b0 + 1;
-                while (b1 < batch.size() && batch[b1].first == batch[b1 - 1].first + 1 &&
-                       h->slots[batch[b1].second].host == h->slots[batch[b1 - 1].second].host + C)
-                    ++b1;
-                const uint64_t x0 = batch[b0].first * C, x1 = std::min(batch[b1 - 1].first * C + C, T);
-                const hipError_t e =
-                    hipMemcpyAsync(dst + x0, h->slots[batch[b0].second].host, x1 - x0, hipMemcpyHostToDevice, st);
-                if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipMemcpyAsync: %s", hipGetErrorString(e));
-                ++calls;
-                b0 = b1;
-            }
-        } else if (max_batch > 1) {
-            const uint8_t* srcs[kGatherBatch];
-            uint64_t ks[kGatherBatch];
-            for (size_t b = 0; b < batch.size(); ++b) {
-                srcs[b] = h->slots[batch[b].second].mapped;
-                ks[b] = batch[b].first;
-            }
-            rc = launch_gather_batch(dst, srcs, ks, (uint32_t)batch.size(), C, T, st);
-            ++calls;
-        } else {
-            const uint64_t k = batch[0].first;
-            const Slot& s0 = h->slots[batch[0].second];
-            ++calls;
-            rc = move_chunk(h, dst, k, s0.host, s0.mapped, std::min(C, T - k * C), si, st);
-        }
-        InFlight f;
-        f.ev = h->slots[batch[0].second].done;  // free: its slot is not in another batch
-        if (rc == SLLM_OK) {
-            hipError_t e = hipEventRecord(f.ev, st);
-            if (e != hipSuccess) rc = fail(SLLM_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-        }
-        for (const auto& item : batch) {
-            f.slots.push_back(item.second);
-            f.bytes += std::min(C, T - item.first * C);
-        }
-        // on error part of the batch may be on the GPU: its slots are not
-        // handed back (the load stops, drains the streams, and the next load
-        // starts from a full free list)
-        if (rc == SLLM_OK) h->inflight.push_back(std::move(f));
-        ++launches;
-        moved += batch.size();
-    }
-    {
-        // after a complete pass every chunk has been read, so no reader waits
-        // for a slot; after an error, stop releases the ones that do
-        std::lock_guard<std::mutex> g(mu);
-        if (rc != SLLM_OK) set_error(rc);
-        stop = true;
-        cv_free.notify_all();
-    }
-    for (auto& t : threads) t.join();
-    h->stats.read_wait_s = wait_s;
-    h->stats.bytes_read = bytes_read;
-    h->stats.bytes_bounced = bytes_bounced;
-    h->stats.n_launches = calls;
-    h->stats.reader_busy_s = (double)busy_ns.load() * 1e-9;
-    h->stats.reader_starved_s = (double)starved_ns.load() * 1e-9;
-    if (err != SLLM_OK) {
-        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);  // drain in-flight copies
-        h->inflight.clear();
-        return fail(err, "%s", err_msg.c_str());
-    }
+    StreamStats ss;
+    const int32_t st = run_stream(plan, read, sink, h->inflight, &ss);
+    h->stats.read_wait_s = ss.wait_s;
+    h->stats.bytes_read = ss.bytes_read;
+    h->stats.bytes_bounced = ss.bytes_bounced;
+    h->stats.n_launches = sink.calls;
+    h->stats.reader_busy_s = ss.reader_busy_s;
+    h->stats.reader_starved_s = ss.reader_starved_s;
+    if (st != SLLM_OK) return st;
     SLLM_TRY(join_streams(h, user));
     if (h->keep) adopt_kept(h);
     return SLLM_OK;
