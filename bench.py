@@ -236,6 +236,59 @@ def storage_peak(path: str, block: int = 4 << 20, depth: int = 32, budget_s: flo
         os.close(fd)
 
 
+def timeline_summary(path: str, T: int):
+    """The streamed pipeline's timeline (written by the library under
+    SLLM_TRACE_FILE) reduced to a few figures per load, then averaged: the
+    share of the load's span during which some reader is reading, during
+    which the GPU holds chunks (moved and not yet seen done), during which
+    both happen, the mean reads and GPU-held chunks in flight, the time to
+    the first move and the drain after the last read."""
+    import csv
+    from collections import defaultdict
+
+    def union(iv):
+        tot, cs, ce = 0.0, None, None
+        for s, e in sorted(iv):
+            if cs is None:
+                cs, ce = s, e
+            elif s <= ce:
+                ce = max(ce, e)
+            else:
+                tot += ce - cs
+                cs, ce = s, e
+        return tot + (ce - cs if cs is not None else 0.0)
+
+    def both(a, b):
+        ev = sorted([(s, 0, 1) for s, _ in a] + [(e, 0, -1) for _, e in a] +
+                    [(s, 1, 1) for s, _ in b] + [(e, 1, -1) for _, e in b])
+        count, last, tot = [0, 0], None, 0.0
+        for t, w, d in ev:
+            if last is not None and count[0] > 0 and count[1] > 0:
+                tot += t - last
+            count[w] += d
+            last = t
+        return tot
+
+    loads = defaultdict(lambda: defaultdict(dict))
+    for r in csv.DictReader(open(path)):
+        loads[r["load"]][int(r["chunk"])][r["event"]] = float(r["t_s"])
+    per = []
+    for chunks in loads.values():
+        reads = [(c["read_begin"], c["read_end"]) for c in chunks.values()]
+        gpu = [(c["moved"], c["done"]) for c in chunks.values()]
+        t0, t1 = min(s for s, _ in reads), max(e for _, e in gpu)
+        span = t1 - t0
+        per.append({"span_ms": span * 1e3, "GBps": T / span / 1e9,
+                    "reading_pct": 100 * union(reads) / span, "gpu_holding_pct": 100 * union(gpu) / span,
+                    "both_pct": 100 * both(reads, gpu) / span,
+                    "reads_in_flight": sum(e - s for s, e in reads) / span,
+                    "chunks_on_gpu": sum(e - s for s, e in gpu) / span,
+                    "first_move_ms": (min(s for s, _ in gpu) - t0) * 1e3,
+                    "drain_ms": (t1 - max(e for _, e in reads)) * 1e3})
+    return {"loads": len(per), "chunks": len(next(iter(loads.values()))) if loads else 0,
+            **{k: round(statistics.mean(p[k] for p in per), 2) for k in per[0]}} if per else None
+
+
 def estimator_replay(ready, T, tiers, dram_bps, storage_bps):
     """Feed the measured steps, in order, to the loading-time estimator
     (q + n / b, refined from each completed load) and report how far each
@@ -491,6 +544,9 @@ def main():
                     help="run the paper's loading ladder (per-tensor reads ... pipeline) on the file instead")
     ap.add_argument("--thread-sweep", action="store_true",
                     help="time the file -> pinned pool stage alone with 1-16 I/O threads instead")
+    ap.add_argument("--trace", default=None,
+                    help="streamed regimes: write the timed loads' pipeline timeline (CSV) to this file and "
+                         "summarize it (tracing waits for each load's last batches)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with one 1 GiB HBM->HBM copy (the counter calibration kernel)")
     args = ap.parse_args()
@@ -574,6 +630,11 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    tracing = bool(args.trace) and not cached
+    if tracing:
+        if os.path.exists(args.trace):
+            os.remove(args.trace)
+        os.environ["SLLM_TRACE_FILE"] = os.path.abspath(args.trace)
     t_start = time.perf_counter()
     for i in range(args.steps):
         r, l, views = step(i)
@@ -581,6 +642,8 @@ def main():
         loads.append(l)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    if tracing:
+        os.environ.pop("SLLM_TRACE_FILE", None)
 
     # sampled parity after timing: tensors' bytes against the generator
     if not args.no_verify:
@@ -603,6 +666,8 @@ def main():
     tiers = binding.TIER_DRAM | (0 if cached else binding.TIER_STORAGE)
     extras["estimator"] = estimator_replay(ready, T, tiers, (h2d_peak or 50.0) * 1e9,
                                            (storage["GBps"] if storage else 5.0) * 1e9)
+    if tracing:
+        extras["timeline"] = timeline_summary(args.trace, T)
     if not cached:
         extras["ring"] = {"io_threads": args.io_threads, "ring_slots": args.ring_slots,
                           "direct_io": int(last_stats.get("direct_io", 0)),

@@ -11,6 +11,7 @@
 //    one event).  A slot is refilled only after its batch's event has fired.
 #include <algorithm>
 #include <atomic>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <deque>
@@ -341,6 +342,33 @@ class GpuSink final : public BatchSink {
     uint32_t max_batch_;
 };
 
+// With SLLM_TRACE_FILE set, each streamed load appends its pipeline
+// timeline to that file as CSV (load, t_s, event, chunk, slot, thread):
+// read_begin / read_end per chunk on its reader thread, moved when the issue
+// loop hands the chunk's batch to the GPU, done when the loop sees the
+// batch's event complete.  Tracing makes the load wait for its last batches.
+const char* trace_path() {
+    const char* s = std::getenv("SLLM_TRACE_FILE");
+    return s && *s ? s : nullptr;
+}
+
+void write_trace(const char* path, std::vector<TraceEvent>& tr) {
+    static std::atomic<uint64_t> loads{0};
+    const uint64_t id = loads.fetch_add(1);
+    std::sort(tr.begin(), tr.end(), [](const TraceEvent& a, const TraceEvent& b) { return a.t < b.t; });
+    FILE* f = std::fopen(path, "a");
+    if (!f) {
+        log_msg(1, "cannot open trace file %s", path);
+        return;
+    }
+    if (std::ftell(f) == 0) std::fprintf(f, "load,t_s,event,chunk,slot,thread\n");
+    static const char* kNames[] = {"read_begin", "read_end", "moved", "done"};
+    for (const TraceEvent& e : tr)
+        std::fprintf(f, "%llu,%.7f,%s,%llu,%u,%u\n", (unsigned long long)id, e.t, kNames[e.kind],
+                     (unsigned long long)e.chunk, e.slot, e.thread);
+    std::fclose(f);
+}
+
 int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     const uint64_t C = h->chunk, T = h->ix.total;
     h->stats.n_chunks = ceil_div(T, C);
@@ -371,6 +399,9 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     auto read = [h](uint64_t k, uint32_t si, uint64_t len, uint64_t* bounced) {
         return read_chunk(h->file, h->slots[si].host, len, k * h->chunk, h->data_path, bounced);
     };
+    std::vector<TraceEvent> trace;
+    const char* tpath = trace_path();
+    if (tpath) plan.trace = &trace;
     StreamStats ss;
     const int32_t st = run_stream(plan, read, sink, h->inflight, &ss);
     h->stats.read_wait_s = ss.wait_s;
@@ -380,6 +411,10 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     h->stats.reader_busy_s = ss.reader_busy_s;
     h->stats.reader_starved_s = ss.reader_starved_s;
     if (st != SLLM_OK) return st;
+    if (tpath) {
+        SLLM_TRY(reclaim_batches(sink, h->inflight, &trace, ss.t_start));
+        write_trace(tpath, trace);
+    }
     SLLM_TRY(join_streams(h, user));
     if (h->keep) adopt_kept(h);
     return SLLM_OK;

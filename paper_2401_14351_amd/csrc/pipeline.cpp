@@ -15,10 +15,14 @@
 
 namespace sllm {
 
-int32_t reclaim_batches(BatchSink& sink, std::deque<InFlightBatch>& inflight) {
+int32_t reclaim_batches(BatchSink& sink, std::deque<InFlightBatch>& inflight, std::vector<TraceEvent>* trace,
+                        double t_start) {
     for (const InFlightBatch& b : inflight) {
         const int32_t st = sink.done(b.token, true);
         if (st < 0) return st;
+        if (trace)
+            for (size_t j = 0; j < b.slots.size(); ++j)
+                trace->push_back({now_s() - t_start, b.chunks[j], b.slots[j], 0, TraceEvent::kDone});
     }
     inflight.clear();
     return SLLM_OK;
@@ -45,6 +49,14 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
     std::string err_msg;
     uint64_t bytes_read = 0, bytes_bounced = 0;
     std::atomic<uint64_t> busy_ns{0}, starved_ns{0};
+    const double t_start = now_s();
+    std::mutex trace_mu;
+    auto trace = [&](TraceEvent::Kind kind, uint64_t k, uint32_t slot, uint32_t thread) {
+        if (!p.trace) return;
+        const double t = now_s() - t_start;
+        std::lock_guard<std::mutex> g(trace_mu);
+        p.trace->push_back({t, k, slot, thread, kind});
+    };
 
     auto set_error = [&](int32_t st) {  // caller holds mu
         if (err == SLLM_OK) {
@@ -58,7 +70,7 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
 
     // a reader takes the next chunk number, a free slot (with keep: slot k),
     // reads the chunk into it and queues it
-    auto reader = [&] {
+    auto reader = [&](uint32_t thread) {
         for (;;) {
             const uint64_t k = next.fetch_add(1);
             if (k >= n) return;
@@ -80,9 +92,11 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
             }
             const uint64_t off = k * C, len = std::min(C, p.read_end - off);
             uint64_t bounced = 0;
+            trace(TraceEvent::kReadBegin, k, si, thread);
             const double r0 = now_s();
             const int32_t st = read(k, si, len, &bounced);
             busy_ns += (uint64_t)((now_s() - r0) * 1e9);
+            if (st == SLLM_OK) trace(TraceEvent::kReadEnd, k, si, thread);
             std::lock_guard<std::mutex> g(mu);
             --reading;
             if (st != SLLM_OK) {
@@ -101,7 +115,7 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
     std::vector<std::thread> threads;
     try {
         threads.reserve(nt);
-        for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader);
+        for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader, i);
     } catch (...) {  // could not start every reader: stop the ones that run
         {
             std::lock_guard<std::mutex> g(mu);
@@ -121,6 +135,8 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
             block = false;
             if (d < 0) return d;
             if (d == 0) break;
+            for (size_t j = 0; j < inflight.front().slots.size(); ++j)
+                trace(TraceEvent::kDone, inflight.front().chunks[j], inflight.front().slots[j], 0);
             if (!p.keep) {  // kept slots are not refilled
                 std::lock_guard<std::mutex> g(mu);
                 for (uint32_t si : inflight.front().slots) free_q.push_back(si);
@@ -189,7 +205,9 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         if (rc == SLLM_OK) {
             for (const ChunkSlot& c : batch) {
                 f.slots.push_back(c.slot);
+                f.chunks.push_back(c.chunk);
                 f.bytes += std::min(C, T - c.chunk * C);
+                trace(TraceEvent::kMoved, c.chunk, c.slot, 0);
             }
             inflight.push_back(std::move(f));
         }
@@ -206,6 +224,7 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
     }
     for (auto& t : threads) t.join();
     if (stats) {
+        stats->t_start = t_start;
         stats->bytes_read = bytes_read;
         stats->bytes_bounced = bytes_bounced;
         stats->batches = seq;

@@ -45,7 +45,18 @@ class BatchSink {
 struct InFlightBatch {
     uint64_t token = 0;
     std::vector<uint32_t> slots;
+    std::vector<uint64_t> chunks;  // chunk held by each slot
     uint64_t bytes = 0;  // partition bytes the batch moves
+};
+
+// One step of one chunk through the pipeline, for the optional timeline.
+struct TraceEvent {
+    enum Kind : uint8_t { kReadBegin = 0, kReadEnd = 1, kMoved = 2, kDone = 3 };
+    double t;        // seconds since the start of run_stream
+    uint64_t chunk;
+    uint32_t slot;
+    uint32_t thread; // reader index for reads, 0 for the issue loop
+    uint8_t kind;
 };
 
 struct StreamPlan {
@@ -57,9 +68,11 @@ struct StreamPlan {
     uint32_t max_batch = 1;   // chunks per move()
     uint64_t target = 1;      // chunks a batch waits to collect while the sink is still busy
     bool keep = false;        // chunk k always uses slot k and slots are never refilled
+    std::vector<TraceEvent>* trace = nullptr;  // when set, every chunk's steps are appended
 };
 
 struct StreamStats {
+    double t_start = 0;       // now_s() when run_stream started (origin of the trace)
     uint64_t bytes_read = 0;
     uint64_t bytes_bounced = 0;
     uint64_t batches = 0;
@@ -72,8 +85,11 @@ struct StreamStats {
 // to *bounced the bytes it staged through a bounce buffer.
 using ChunkReader = std::function<int32_t(uint64_t k, uint32_t slot, uint64_t len, uint64_t* bounced)>;
 
-// Wait for every batch still in flight (from an earlier load) and forget it.
-int32_t reclaim_batches(BatchSink& sink, std::deque<InFlightBatch>& inflight);
+// Wait for every batch still in flight (from an earlier load) and forget it;
+// with a trace, append each chunk's kDone at `t` seconds after `t_start`
+// (the now_s() value run_stream started at, StreamStats::t_start).
+int32_t reclaim_batches(BatchSink& sink, std::deque<InFlightBatch>& inflight,
+                        std::vector<TraceEvent>* trace = nullptr, double t_start = 0);
 
 // Stream every chunk of the partition through the ring into the sink.
 // Batches still in flight when it returns stay in `inflight` (their slots

@@ -11,7 +11,10 @@
 //   * a reader never writes a slot that a batch not yet complete still holds
 //     (the slot-recycling rule; ThreadSanitizer checks the same ordering);
 //   * an injected read error or move() error is returned with its message,
-//     leaves nothing in flight, and the next load on the same sink succeeds.
+//     leaves nothing in flight, and the next load on the same sink succeeds;
+//   * the optional timeline has every chunk read, moved and done once, in
+//     that order, and no slot read again before its previous chunk was done.
+#include <algorithm>
 #include <atomic>
 #include <chrono>
 #include <condition_variable>
@@ -145,6 +148,33 @@ class CpuSink final : public BatchSink {
     std::thread worker_;
 };
 
+// The timeline of one clean load: every chunk read, moved and done once, in
+// that order, and a slot read again only after the chunk it held was done.
+int check_trace(const std::vector<TraceEvent>& tr, uint64_t n, uint32_t n_slots) {
+    std::vector<double> t[4];
+    for (auto& v : t) v.assign(n, -1);
+    std::vector<uint32_t> slot_of(n, 0);
+    for (const TraceEvent& e : tr) {
+        if (e.chunk >= n || e.kind > 3 || e.slot >= n_slots) return 1;
+        if (t[e.kind][e.chunk] >= 0) return 2;  // a step recorded twice
+        t[e.kind][e.chunk] = e.t;
+        if (e.kind == TraceEvent::kReadBegin) slot_of[e.chunk] = e.slot;
+    }
+    std::vector<std::vector<std::pair<double, double>>> uses(n_slots);
+    for (uint64_t k = 0; k < n; ++k) {
+        for (int s = 0; s < 4; ++s)
+            if (t[s][k] < 0) return 3;  // a step missing
+        if (!(t[0][k] <= t[1][k] && t[1][k] <= t[2][k] && t[2][k] <= t[3][k])) return 4;
+        uses[slot_of[k]].push_back({t[0][k], t[3][k]});
+    }
+    for (auto& u : uses) {
+        std::sort(u.begin(), u.end());
+        for (size_t i = 1; i < u.size(); ++i)
+            if (u[i].first < u[i - 1].second) return 5;  // refilled before its chunk was done
+    }
+    return 0;
+}
+
 struct Case {
     uint64_t T, C;
     uint32_t slots, threads, max_batch;
@@ -203,6 +233,8 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
             std::printf("reclaim failed: %s\n", sllm_last_error());
             return 1;
         }
+        std::vector<TraceEvent> trace;
+        plan.trace = faulty || load % 2 ? nullptr : &trace;
         StreamStats ss;
         st = run_stream(plan, read, sink, inflight, &ss);
         if (faulty) {
@@ -225,8 +257,15 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
             std::printf("load %d failed: %d %s\n", load, st, sllm_last_error());
             return 1;
         }
-        st = reclaim_batches(sink, inflight);  // the GPU path's stream join
+        st = reclaim_batches(sink, inflight, plan.trace, ss.t_start);  // the GPU path's stream join
         if (st != SLLM_OK || !inflight.empty()) return 1;
+        if (plan.trace) {
+            const int bad = check_trace(trace, n, n_slots);
+            if (bad) {
+                std::printf("load %d: timeline check %d failed (%zu events)\n", load, bad, trace.size());
+                return 1;
+            }
+        }
         if (ss.bytes_read != cs.T) {
             std::printf("read %llu bytes of %llu\n", (unsigned long long)ss.bytes_read, (unsigned long long)cs.T);
             return 1;

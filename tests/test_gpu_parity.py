@@ -429,6 +429,44 @@ def test_gather_shapes(torch_cuda, opt125m, shape, monkeypatch):
 
 
 @pytest.mark.parametrize("engine", ["kernel", "sdma"])
+def test_pipeline_timeline(torch_cuda, opt125m, tmp_path, monkeypatch, engine):
+    """SLLM_TRACE_FILE: each streamed load appends its timeline; every chunk
+    is read, moved and done once, in that order, and a slot is read again
+    only after the chunk it held is done.  The loads stay byte-exact."""
+    import csv
+
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, _ = expected(tensors, spec.alignment)
+    path = tmp_path / "trace.csv"
+    monkeypatch.setenv("SLLM_TRACE_FILE", str(path))
+    C = 1 << 20
+    with binding.Checkpoint(d, engine=engine, chunk_size=C, ring_slots=8, io_threads=4) as ck:
+        for rep in range(2):
+            assert_same(run_load(torch, ck, len(want)), want, f"traced load {rep}")
+    n = -(-len(want) // C)
+    rows = list(csv.DictReader(open(path)))
+    loads = sorted({r["load"] for r in rows})
+    assert len(loads) == 2
+    for ld in loads:
+        t = {}
+        for r in rows:
+            if r["load"] == ld:
+                key = (int(r["chunk"]), r["event"])
+                assert key not in t, f"{key} recorded twice"
+                t[key] = (float(r["t_s"]), int(r["slot"]))
+        assert len(t) == 4 * n
+        uses = {}
+        for k in range(n):
+            times = [t[(k, e)][0] for e in ("read_begin", "read_end", "moved", "done")]
+            assert times == sorted(times), (k, times)
+            uses.setdefault(t[(k, "read_begin")][1], []).append((times[0], times[3]))
+        for slot, u in uses.items():
+            u.sort()
+            assert all(b[0] >= a[1] for a, b in zip(u, u[1:])), f"slot {slot} refilled before its chunk was done"
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
 @pytest.mark.parametrize("C", [64 << 10, (64 << 10) + 48, 1 << 20])
 def test_streamed_batches(torch_cuda, opt125m, engine, C):
     """Many small chunks through a deep ring: the issue loop moves every
