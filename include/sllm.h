@@ -282,6 +282,8 @@ typedef struct sllm_stats {
     double   reader_starved_s;  /* streamed loads: I/O-thread time spent waiting
                                    for a free slot (summed over threads)       */
 } sllm_stats;
+/* Counters of the handle's last load.  With SLLM_OPEN_TIMING this waits for
+ * that load's device work to finish (to read its events).  Errors: INVAL, HIP. */
 int32_t sllm_get_stats(const sllm_ckpt* h, sllm_stats* out);
 
 /* =========================================================================
