@@ -100,7 +100,10 @@ int32_t sllm_convert(const sllm_src_tensor* tensors, uint64_t n,
  * memory twice: tensors are added one at a time and written immediately.
  * The files it produces are byte-identical to sllm_convert's.
  * sllm_writer_close writes the index and frees the writer (even on error);
- * sllm_writer_abort removes the partial files and frees the writer. */
+ * sllm_writer_abort removes the partial files and frees the writer.
+ * Errors: as sllm_convert; after a failed sllm_writer_add the writer only
+ * accepts sllm_writer_abort or sllm_writer_close (which then removes the
+ * files and returns the error). */
 typedef struct sllm_writer sllm_writer;
 int32_t sllm_writer_open(const char* out_dir, const sllm_convert_opts* opts,
                          sllm_writer** out);
@@ -144,6 +147,7 @@ typedef struct sllm_pool_info {
     uint64_t free_chunks;
     uint64_t cached_checkpoints;
 } sllm_pool_info;
+/* Sizes and occupancy of the pool.  Errors: INVAL (NULL argument). */
 int32_t sllm_pool_query(const sllm_pool* pool, sllm_pool_info* out);
 
 /* Read the whole partition of checkpoint directory `dir` into pool chunks,
@@ -216,7 +220,8 @@ typedef struct sllm_ckpt sllm_ckpt;
  * Errors: INVAL, IO, FORMAT, NOMEM, HIP. */
 int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out);
 
-/* Bytes a load writes: T (file layout) or T2 (dev_alignment != 0). */
+/* Bytes a load writes: T (file layout) or T2 (dev_alignment != 0); 0 for a
+ * NULL handle. */
 uint64_t sllm_total_bytes(const sllm_ckpt* h);
 
 /* Load the checkpoint into device memory [dev_dst, dev_dst + total_bytes).
@@ -254,11 +259,12 @@ typedef struct sllm_tensor_info {
 } sllm_tensor_info;
 
 /* Copy up to `cap` entries, in layout order, into out[] and set *n_total to
- * the number of tensors (cap = 0 with out = NULL asks for the count only). */
+ * the number of tensors (cap = 0 with out = NULL asks for the count only).
+ * Errors: INVAL (NULL handle, or out NULL with cap > 0). */
 int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, uint64_t cap,
                           uint64_t* n_total);
 
-/* Look one tensor up by name.  NOTFOUND if absent. */
+/* Look one tensor up by name.  Errors: INVAL (NULL argument), NOTFOUND. */
 int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_tensor_info* out);
 
 typedef struct sllm_stats {
@@ -325,13 +331,15 @@ typedef struct sllm_import sllm_import;
  * Errors: INVAL (not device memory, allocation too large, range outside it), HIP. */
 int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32_t device, void* stream,
                            sllm_ipc_desc* desc, sllm_export** out);
+/* Release the export (its event and descriptor); importers must have
+ * closed their mappings.  Errors: HIP. */
 int32_t sllm_export_destroy(sllm_export* ex);
 
 /* Map an exported buffer into this process: *dev_ptr is its start here, and
  * `stream` waits (on the device) for the exporter's handoff event, so work
  * queued on it afterwards sees the loaded bytes.  Errors: INVAL, HIP. */
 int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, void** dev_ptr, sllm_import** out);
-/* Unmap; work that reads the buffer must have finished. */
+/* Unmap; work that reads the buffer must have finished.  Errors: HIP. */
 int32_t sllm_import_close(sllm_import* im);
 
 /* =========================================================================
@@ -349,13 +357,15 @@ int32_t sllm_import_close(sllm_import* im);
 typedef struct sllm_estimator sllm_estimator;
 
 /* Initial bandwidths in bytes per second (> 0) and the weight in (0, 1] of a
- * new measurement in the running estimate (1 = keep only the latest). */
+ * new measurement in the running estimate (1 = keep only the latest).
+ * Errors: INVAL, NOMEM. */
 int32_t sllm_estimator_create(double dram_bytes_per_s, double storage_bytes_per_s, double weight,
                               sllm_estimator** out);
 void    sllm_estimator_destroy(sllm_estimator* e);
 
 /* q + n / b for a load of `bytes` crossing `tiers` (SLLM_TIER_* bits),
- * queued behind every load enqueued and not yet completed. */
+ * queued behind every load enqueued and not yet completed.  Errors: INVAL
+ * (NULL argument, no or unknown tier bits). */
 int32_t sllm_estimator_query(const sllm_estimator* e, uint64_t bytes, uint32_t tiers, double* eta_s);
 
 /* Queue such a load: *eta_s is its estimate (as for query) and *task its id;
@@ -368,10 +378,11 @@ int32_t sllm_estimator_enqueue(sllm_estimator* e, uint64_t bytes, uint32_t tiers
  * task, INVAL for seconds <= 0. */
 int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, double seconds);
 
-/* Current bandwidth estimate of one tier (bytes per second). */
+/* Current bandwidth estimate of one tier (bytes per second).  Errors: INVAL. */
 int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bytes_per_s);
 
-/* Close the handle; waits for its in-flight device work first. */
+/* Close the handle; waits for its in-flight device work first.  NULL is a
+ * no-op.  Errors: BUSY (a load is running on the handle). */
 int32_t sllm_close(sllm_ckpt* h);
 
 /* Message of the last failed call on this thread ("" if none). */
