@@ -331,15 +331,16 @@ typedef struct sllm_import sllm_import;
  * Errors: INVAL (not device memory, allocation too large, range outside it), HIP. */
 int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32_t device, void* stream,
                            sllm_ipc_desc* desc, sllm_export** out);
-/* Release the export (its event and descriptor); importers must have
- * closed their mappings.  Errors: HIP. */
+/* Release the export (its handoff event); importers must have closed their
+ * mappings.  NULL is a no-op.  Always returns SLLM_OK. */
 int32_t sllm_export_destroy(sllm_export* ex);
 
 /* Map an exported buffer into this process: *dev_ptr is its start here, and
  * `stream` waits (on the device) for the exporter's handoff event, so work
  * queued on it afterwards sees the loaded bytes.  Errors: INVAL, HIP. */
 int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, void** dev_ptr, sllm_import** out);
-/* Unmap; work that reads the buffer must have finished.  Errors: HIP. */
+/* Unmap; work that reads the buffer must have finished.  NULL is a no-op.
+ * Errors: HIP (the mapping could not be closed; the import is freed anyway). */
 int32_t sllm_import_close(sllm_import* im);
 
 /* =========================================================================
