@@ -594,7 +594,8 @@ def main():
     cached = args.regime == "dram"
     t0 = time.time()
     pool = binding.Pool(C, n_chunks if cached else args.ring_slots)
-    log(f"pinned pool: {n_chunks if cached else args.ring_slots} x {C / 2**20:g} MiB in {time.time() - t0:.1f} s")
+    pool_alloc_s = time.time() - t0
+    log(f"pinned pool: {n_chunks if cached else args.ring_slots} x {C / 2**20:g} MiB in {pool_alloc_s:.1f} s")
     fill_s = None
     if cached:
         t0 = time.time()
@@ -605,7 +606,10 @@ def main():
     if not cached:
         open_kw.update(chunk_size=C, io_threads=args.io_threads, ring_slots=args.ring_slots,
                        direct_io=args.regime == "direct")
+    t0 = time.perf_counter()
     buf = torch.empty(T, dtype=torch.uint8, device="cuda:0")
+    torch.cuda.synchronize()
+    hbm_alloc_s = time.perf_counter() - t0
     last_stats = {}
 
     ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -656,6 +660,9 @@ def main():
     del views
     extras = ({} if (args.no_extras or not cached or args.dev_alignment) else
               measure_extras(torch, spec, d, pool, buf, stream, args.engine))
+    # one-time set-up outside time-to-ready, as a model manager that keeps its
+    # pinned pool and HBM buffer pays it once
+    extras["setup"] = {"pinned_pool_alloc_s": round(pool_alloc_s, 3), "hbm_buffer_alloc_s": round(hbm_alloc_s, 4)}
     if fill_s is not None:
         extras["dram_tier_fill"] = {"GBps": round(T / fill_s / 1e9, 3), "s": round(fill_s, 3),
                                     "io_threads": args.io_threads, "source": "converted file, page cache warm"}
