@@ -1,0 +1,113 @@
+"""Seeded random sweep of load configurations on small checkpoints: file
+alignment, device alignment, engine, cached or streamed (buffered or direct
+reads, kept slots), chunk size, ring size and reader count drawn at random,
+every byte of every load compared with the oracle's image and a sentinel
+past it.  Each configuration is printed before it runs."""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2401_14351_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = 0x3C
+N_CONFIGS = 600
+
+
+def say(*a):
+    print("[gpu-rand]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    binding.lib()
+    return torch
+
+
+def draw(rng):
+    A = int(rng.choice([1, 2, 4, 16, 256, 4096]))
+    A2 = int(rng.choice([0, 0, 16, 32, 256, 4096]))
+    engine = str(rng.choice(["kernel", "sdma"]))
+    source = str(rng.choice(["cached", "streamed", "streamed", "direct", "keep"]))
+    if source == "direct":
+        C = 4096 * int(rng.integers(1, 65))
+    else:
+        C = int(rng.choice([16, 48, 4096, 65536, 1 << 20, 16 * int(rng.integers(1, 5000)),
+                            int(rng.integers(1, 100000))]))
+    kind = str(rng.choice(["tiny", "stress"]))
+    seed = int(rng.integers(0, 1 << 30))
+    if kind == "tiny":
+        spec = synth.tiny(seed, n=int(rng.integers(1, 40)), alignment=A, max_bytes=int(rng.integers(1, 200_000)))
+    else:
+        spec = synth.stress(n=int(rng.integers(1, 200)), seed=seed, min_bytes=1,
+                            max_bytes=int(rng.integers(2, 1 << 20)))
+    return dict(A=A, A2=A2, engine=engine, source=source, C=C, kind=kind, seed=seed, spec=spec,
+                ring=int(rng.integers(1, 9)), io=int(rng.integers(1, 5)))
+
+
+def test_random_configurations(torch_cuda, tmp_path):
+    torch = torch_cuda
+    rng = np.random.default_rng(20240114)
+    for i in range(N_CONFIGS):
+        cfg = draw(rng)
+        spec = cfg.pop("spec")
+        say(i, cfg)
+        tensors = [(t.name, t.dtype, t.shape, d) for t, d in zip(spec.tensors, synth.materialize(spec, threads=4))]
+        A, A2 = cfg["A"], cfg["A2"]
+        # at most 2048 chunks (every pool chunk takes at least 4 KiB of pinned memory)
+        _, T = oracle.plan_layout([t.nbytes for t in spec.tensors], A)
+        C = max(cfg["C"], -(-T // 2048))
+        if cfg["source"] == "direct":
+            C = -(-C // 4096) * 4096
+        cfg["C"] = C
+        say(i, "T", T, "C", C)
+        d = str(tmp_path / f"c{i}")
+        os.makedirs(d)
+        binding.convert(iter(tensors), d, A, C)
+        index = oracle.make_index(tensors, A, C)
+        want = bytes(oracle.partition_bytes(tensors, A)[:index.total_bytes])
+        if A2:
+            want = bytes(oracle.repack(want, index, A2))
+        n_chunks = max(1, -(-index.total_bytes // C))
+        pool = None
+        kw = dict(engine=cfg["engine"], dev_alignment=A2)
+        if cfg["source"] == "cached":
+            pool = binding.Pool(C, n_chunks)
+            pool.cache(d, io_threads=cfg["io"])
+            kw.update(pool=pool)
+        elif cfg["source"] == "keep":
+            pool = binding.Pool(C, n_chunks)
+            kw.update(pool=pool, cache=True, io_threads=cfg["io"])
+        else:
+            kw.update(chunk_size=C, ring_slots=cfg["ring"], io_threads=cfg["io"], direct_io=cfg["source"] == "direct")
+        try:
+            with binding.Checkpoint(d, **kw) as ck:
+                assert ck.total_bytes == len(want)
+                for rep in range(2):
+                    buf = torch.full((len(want) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+                    ck.load_into(buf)
+                    torch.cuda.synchronize()
+                    host = buf.cpu().numpy()
+                    assert (host[len(want):] == SENTINEL).all(), f"config {i}: bytes past the image written"
+                    got = host[:len(want)].tobytes()
+                    if got != want:
+                        a = np.frombuffer(got, np.uint8)
+                        b = np.frombuffer(want, np.uint8)
+                        bad = np.nonzero(a != b)[0]
+                        raise AssertionError(f"config {i} {cfg} load {rep}: {bad.size} bytes differ, "
+                                             f"first at {bad[:8].tolist()}")
+        finally:
+            if pool is not None:
+                if cfg["source"] in ("cached", "keep") and pool.info()["cached_checkpoints"]:
+                    pool.evict(d)
+                pool.close()
