@@ -1,7 +1,8 @@
 """Seeded random sweep of load configurations on small checkpoints: file
 alignment, device alignment, engine, cached or streamed (buffered or direct
 reads, kept slots), chunk size, ring size and reader count drawn at random,
-every byte of every load compared with the oracle's image and a sentinel
+every byte of every load (and, with a device alignment, of the HBM repack
+of the file-layout image) compared with the oracle's image and a sentinel
 past it.  Each configuration is printed before it runs."""
 
 import os
@@ -75,9 +76,8 @@ def test_random_configurations(torch_cuda, tmp_path):
         os.makedirs(d)
         binding.convert(iter(tensors), d, A, C)
         index = oracle.make_index(tensors, A, C)
-        want = bytes(oracle.partition_bytes(tensors, A)[:index.total_bytes])
-        if A2:
-            want = bytes(oracle.repack(want, index, A2))
+        image = bytes(oracle.partition_bytes(tensors, A)[:index.total_bytes])
+        want = bytes(oracle.repack(image, index, A2)) if A2 else image
         n_chunks = max(1, -(-index.total_bytes // C))
         pool = None
         kw = dict(engine=cfg["engine"], dev_alignment=A2)
@@ -106,6 +106,14 @@ def test_random_configurations(torch_cuda, tmp_path):
                         bad = np.nonzero(a != b)[0]
                         raise AssertionError(f"config {i} {cfg} load {rep}: {bad.size} bytes differ, "
                                              f"first at {bad[:8].tolist()}")
+                if A2:  # the HBM repack of the file-layout image gives the same bytes
+                    src = torch.frombuffer(bytearray(image + bytes(16)), dtype=torch.uint8).to("cuda:0")
+                    out = torch.full((len(want) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+                    ck.repack(src, out)
+                    torch.cuda.synchronize()
+                    host = out.cpu().numpy()
+                    assert (host[len(want):] == SENTINEL).all(), f"config {i}: repack wrote past the image"
+                    assert host[:len(want)].tobytes() == want, f"config {i} {cfg}: repack differs"
         finally:
             if pool is not None:
                 if cfg["source"] in ("cached", "keep") and pool.info()["cached_checkpoints"]:
