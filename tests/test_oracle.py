@@ -269,6 +269,27 @@ def test_index_fields_at_documented_positions():
     assert pos == len(blob) - 4
 
 
+def test_crc_is_the_ieee_polynomial():
+    """The index trailer's CRC-32 is the IEEE 802.3 one (reflected 0xEDB88320,
+    initial and final 0xFFFFFFFF): its published check value over the ASCII
+    digits 1-9 is 0xCBF43926, and a bitwise long division written out here
+    agrees with zlib.crc32 on random data."""
+    assert zlib.crc32(b"123456789") == 0xCBF43926
+
+    def crc_bitwise(data):
+        c = 0xFFFFFFFF
+        for byte in data:
+            c ^= byte
+            for _ in range(8):
+                c = (c >> 1) ^ (0xEDB88320 if c & 1 else 0)
+        return c ^ 0xFFFFFFFF
+
+    rng = np.random.default_rng(9)
+    for n in (0, 1, 7, 64, 1000):
+        data = rng.integers(0, 256, n, dtype=np.uint8).tobytes()
+        assert crc_bitwise(data) == zlib.crc32(data)
+
+
 def test_index_round_trip_and_damage():
     index, _ = _tiny_converted(A=16, seed=7)
     blob = oracle.encode_index(index)
