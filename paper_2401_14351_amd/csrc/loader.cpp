@@ -361,6 +361,7 @@ void write_trace(const char* path, std::vector<TraceEvent>& tr) {
         log_msg(1, "cannot open trace file %s", path);
         return;
     }
+    std::fseek(f, 0, SEEK_END);
     if (std::ftell(f) == 0) std::fprintf(f, "load,t_s,event,chunk,slot,thread\n");
     static const char* kNames[] = {"read_begin", "read_end", "moved", "done"};
     for (const TraceEvent& e : tr)
