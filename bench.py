@@ -514,6 +514,32 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
         "first_from_cache": int(first["from_cache"]), "second_GBps": round(T / (t2 - t1) / 1e9, 3),
         "second_from_cache": int(second["from_cache"]), "cached_after": pool.info()["cached_checkpoints"]}
     log("file then cached:", out["file_direct_then_cached"])
+    # the one-time conversion (Sec. 4.1; reported, not graded): the first
+    # tensors of the workload, about 1 GiB held in memory, written by the
+    # batch converter and by the streaming writer, each with fsync
+    import shutil
+    import tempfile
+
+    k, nbytes = 0, 0
+    while k < len(spec.tensors) and nbytes < (1 << 30):
+        nbytes += spec.tensors[k].nbytes
+        k += 1
+    sub = [(t.name, t.dtype, t.shape, data) for _, t, data in synth.iter_tensors(spec, indices=range(k))]
+    tmp = tempfile.mkdtemp(dir=os.path.dirname(os.path.abspath(d)))
+    try:
+        t0 = time.perf_counter()
+        binding.convert_array(sub, os.path.join(tmp, "batch"), spec.alignment, spec.chunk_size, fsync=True)
+        t_batch = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        binding.convert(iter(sub), os.path.join(tmp, "stream"), spec.alignment, spec.chunk_size, fsync=True)
+        t_stream = time.perf_counter() - t0
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+    del sub
+    out["convert"] = {"tensors": k, "bytes": nbytes, "batch_GBps": round(nbytes / t_batch / 1e9, 3),
+                      "streaming_GBps": round(nbytes / t_stream / 1e9, 3), "fsync": True,
+                      "device": block_device(d)}
+    log("convert:", out["convert"])
     return out
 
 

@@ -225,7 +225,7 @@ def convert(tensors: Iterable[Tuple[str, str, Sequence[int], object]], out_dir: 
 
 
 def convert_array(tensors: Sequence[Tuple[str, str, Sequence[int], object]], out_dir: str, alignment: int = 256,
-                  chunk_size: int = 16 << 20) -> None:
+                  chunk_size: int = 16 << 20, fsync: bool = False) -> None:
     """``sllm_convert`` over a list held in memory."""
     L = lib()
     structs, keep = [], []
@@ -234,7 +234,7 @@ def convert_array(tensors: Sequence[Tuple[str, str, Sequence[int], object]], out
         structs.append(st)
         keep.append(k)
     arr = (SrcTensor * max(1, len(structs)))(*structs)
-    opts = ConvertOpts(alignment, chunk_size, 0, 0)
+    opts = ConvertOpts(alignment, chunk_size, CONVERT_FSYNC if fsync else 0, 0)
     os.makedirs(out_dir, exist_ok=True)
     check(L.sllm_convert(arr, len(structs), out_dir.encode(), C.byref(opts)))
 
