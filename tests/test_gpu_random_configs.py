@@ -17,7 +17,9 @@ from paper_2401_14351_amd import binding, synth
 pytestmark = pytest.mark.gpu
 
 SENTINEL = 0x3C
-N_CONFIGS = 600
+# a longer or different sweep: SLLM_RAND_CONFIGS=5000 SLLM_RAND_SEED=7
+N_CONFIGS = int(os.environ.get("SLLM_RAND_CONFIGS", "600"))
+SEED = int(os.environ.get("SLLM_RAND_SEED", "20240114"))
 
 
 def say(*a):
@@ -58,7 +60,7 @@ def draw(rng):
 
 def test_random_configurations(torch_cuda, tmp_path):
     torch = torch_cuda
-    rng = np.random.default_rng(20240114)
+    rng = np.random.default_rng(SEED)
     for i in range(N_CONFIGS):
         cfg = draw(rng)
         spec = cfg.pop("spec")
