@@ -29,7 +29,7 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2401_14351_amd import binding, synth  # noqa: E402
+from paper_2401_14351_amd import binding, synth, verify  # noqa: E402
 
 METRIC = "checkpoint load GB/s host DRAM→HBM + time-to-ready (s), 7B-shaped bf16"
 PCIE_GEN5_X16_GBPS = 64.0   # MI355X host link: PCIe 5.0 x16, 32 GT/s x 16 lanes per direction
@@ -78,24 +78,42 @@ def log(*a):
 
 def spec_key(spec) -> str:
     h = hashlib.sha256()
-    h.update(f"{spec.name}/{spec.seed}/{spec.alignment}/{spec.chunk_size}".encode())
+    h.update(f"{spec.name}/{spec.seed}/{spec.alignment}/{spec.chunk_size}/{synth.BLOCK}".encode())
     for t in spec.tensors:
         h.update(f"{t.name}:{t.dtype}:{t.shape}:{t.init};".encode())
     return h.hexdigest()[:16]
 
 
-def ensure_checkpoint(spec, d: str) -> None:
-    """Generate and convert the synthetic checkpoint unless it already exists."""
+def ensure_checkpoint(spec, d: str):
+    """Generate and convert the synthetic checkpoint unless it already
+    exists; return the digests of its tensors' generator bytes (computed
+    while converting, or regenerated if a converted copy has none)."""
     marker = os.path.join(d, "bench.key")
     key = spec_key(spec)
     if os.path.exists(marker) and open(marker).read() == key:
-        return
+        digests = verify.load_digests(d, key, len(spec.tensors))
+        if digests is None:
+            t0 = time.time()
+            digests = verify.generated_digests(spec)
+            verify.save_digests(d, key, digests)
+            log(f"digests of {spec.name} regenerated in {time.time() - t0:.1f} s")
+        return digests
     os.makedirs(d, exist_ok=True)
+    if os.path.exists(marker):
+        os.remove(marker)
     t0 = time.time()
-    gen = ((t.name, t.dtype, t.shape, data) for _, t, data in synth.iter_tensors(spec))
-    binding.convert(gen, d, spec.alignment, spec.chunk_size, fsync=True)
+    digests = []
+
+    def tensors():
+        for _, t, data, dg in verify.generate(spec):
+            digests.append(dg)
+            yield t.name, t.dtype, t.shape, data
+
+    binding.convert(tensors(), d, spec.alignment, spec.chunk_size, fsync=True)
+    verify.save_digests(d, key, digests)
     open(marker, "w").write(key)
     log(f"converted {spec.name} into {d} in {time.time() - t0:.1f} s")
+    return digests
 
 
 def measure_peaks(torch, nbytes: int = 1 << 30, reps: int = 5):
@@ -584,7 +602,7 @@ def main():
 
     spec = synth.config(args.workload)
     d = args.dir or os.path.join(os.environ.get("SLLM_BENCH_DIR", "/tmp/sllm_bench"), spec.name)
-    ensure_checkpoint(spec, d)
+    digests = ensure_checkpoint(spec, d)
     cpu = None if args.no_cpu_baseline else cpu_baseline(d, args.cpu_budget)  # before any GPU work
     if cpu:
         log("cpu baseline:", cpu["sample"], cpu["value"], "GB/s")
@@ -675,15 +693,22 @@ def main():
     if tracing:
         os.environ.pop("SLLM_TRACE_FILE", None)
 
-    # sampled parity after timing: tensors' bytes against the generator
-    if not args.no_verify:
-        names = [t.name for t in spec.tensors]
-        for i in sorted({0, 1, len(names) // 2, len(names) - 2, len(names) - 1}):
-            got = views[names[i]].contiguous().view(torch.uint8).cpu().numpy().reshape(-1)
-            want = synth.tensor_bytes(spec, i)
-            if got.tobytes() != want.tobytes():
-                raise SystemExit(f"bench: tensor {names[i]} differs from the generator's bytes")
+    # after timing, every byte of the last step's image: each tensor's bytes
+    # at the offset the library's index gives equal the generator's, every
+    # other byte of [0, T) is zero
     del views
+    parity = None
+    if not args.no_verify:
+        with binding.Checkpoint(d, index_only=True, dev_alignment=args.dev_alignment) as probe:
+            offsets = [t.offset for t in probe.tensors()]
+        t0 = time.perf_counter()
+        try:
+            got = verify.check_image(torch, buf, spec, offsets, T, digests)
+        except verify.Mismatch as e:
+            raise SystemExit(f"bench: the loaded image differs from the generator's bytes: {e}")
+        parity = {"checked": "every byte of the last timed step's image", **got,
+                  "s": round(time.perf_counter() - t0, 2)}
+        log("parity:", parity)
     extras = ({} if (args.no_extras or not cached or args.dev_alignment) else
               measure_extras(torch, spec, d, pool, buf, stream, args.engine))
     # one-time set-up outside time-to-ready, as a model manager that keeps its
@@ -755,6 +780,7 @@ def main():
                      "hbm_copy_measured": None if hbm_peak is None else round(hbm_peak, 1),
                      "link": next((f"{g['speed']} x{g['width']}" for g in gpu_links()), None)},
         "cpu_baseline": cpu,
+        "parity": parity,
         "extras": extras,
     }
     print(json.dumps(out), flush=True)

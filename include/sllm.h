@@ -229,8 +229,9 @@ uint64_t sllm_total_bytes(const sllm_ckpt* h);
  * included (as zero); bytes past it are untouched.  Returns once every file
  * read has finished and every copy or kernel has been enqueued; completion is
  * ordered on `stream`: work queued there after this call sees every byte.
- * Errors: INVAL (dev_dst is not device memory of the handle's device, or
- * not 16-byte aligned), RANGE (dst_bytes < total, or the range runs past the
+ * Errors: INVAL (dev_dst is not device memory of the handle's device, is
+ * memory whose allocation range the runtime cannot report, or is not
+ * 16-byte aligned), RANGE (dst_bytes < total, or the range runs past the
  * end of dev_dst's allocation), IO, HIP, BUSY (another load on this
  * handle).  On error, in-flight work is drained and the destination's
  * contents are unspecified; the handle stays usable. */
@@ -242,7 +243,8 @@ int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream)
  * dev_alignment.  src and dst are device pointers, 16-byte aligned, and must
  * not overlap.  Enqueued on `stream`.
  * Errors: INVAL (handle opened without dev_alignment, overlap, a buffer that
- * is not device memory of the handle's device), RANGE, HIP. */
+ * is not device memory of the handle's device or whose allocation range the
+ * runtime cannot report), RANGE, HIP. */
 int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes,
                     void* dst_dev, uint64_t dst_bytes, void* stream);
 
@@ -337,7 +339,9 @@ int32_t sllm_export_destroy(sllm_export* ex);
 
 /* Map an exported buffer into this process: *dev_ptr is its start here, and
  * `stream` waits (on the device) for the exporter's handoff event, so work
- * queued on it afterwards sees the loaded bytes.  Errors: INVAL, HIP. */
+ * queued on it afterwards sees the loaded bytes.  Errors: INVAL (unknown
+ * flags, or offset + bytes past the end of the mapped allocation: nothing
+ * stays mapped), HIP. */
 int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, void** dev_ptr, sllm_import** out);
 /* Unmap; work that reads the buffer must have finished.  NULL is a no-op.
  * Errors: HIP (the mapping could not be closed; the import is freed anyway). */

@@ -351,7 +351,9 @@ class Checkpoint:
         check(lib().sllm_load(self._h, dst_ptr, dst_bytes, _stream_ptr(stream)))
 
     def load_into(self, buf, stream=None) -> None:
-        """Load into a uint8 torch tensor on the handle's device."""
+        """Load into a contiguous uint8 torch tensor on the handle's device
+        (it may be a slice of a larger allocation)."""
+        _check_buffer(buf)
         self.load(buf.data_ptr(), buf.numel(), stream)
 
     def load_with_views(self, buf, stream=None, after_load: Optional[Callable[[], None]] = None):
@@ -392,6 +394,8 @@ class Checkpoint:
         return out
 
     def repack(self, src, dst, stream=None) -> None:
+        _check_buffer(src)
+        _check_buffer(dst)
         check(lib().sllm_repack(self._h, src.data_ptr(), src.numel(), dst.data_ptr(), dst.numel(),
                                 _stream_ptr(stream)))
 
@@ -412,26 +416,43 @@ class Checkpoint:
         self.close()
 
 
+def _check_buffer(buf) -> None:
+    """Device buffers handed to the library are flat runs of bytes: the C ABI
+    sees only data_ptr() and numel(), so anything else would be misread."""
+    import torch
+
+    if buf.dtype != torch.uint8 or buf.dim() != 1 or not buf.is_contiguous():
+        raise ValueError(f"expected a contiguous 1-d uint8 tensor, got {buf.dtype} with shape "
+                         f"{tuple(buf.shape)} and strides {buf.stride()}")
+
+
 def views(buf, tensors: Sequence[Tensor]) -> Dict[str, object]:
     """torch views of each tensor at base + offset in ``buf`` (uint8).
 
-    A tensor whose offset is not a multiple of its element size (only in a
-    dense file layout, A < itemsize) is returned as its raw uint8 bytes."""
+    ``buf`` may start anywhere inside its storage (a slice of a larger
+    allocation): offsets count from ``buf``'s first byte.  A tensor whose
+    address is not a multiple of its element size (a dense file layout,
+    A < itemsize, or a buffer that starts off that alignment) is returned as
+    its raw uint8 bytes."""
     import torch
 
+    _check_buffer(buf)
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8}
     typed = {}
     out = {}
     for t in tensors:
         isz = ITEMSIZE[DTYPE_CODE[t.dtype]]
-        if t.offset % isz:
+        if buf.storage_offset() % isz or t.offset % isz:
             out[t.name] = buf[t.offset:t.offset + t.nbytes]
             continue
         base = typed.get(t.dtype)
         if base is None:
             base = buf[: (buf.numel() // isz) * isz].view(tdt[t.dtype])
             typed[t.dtype] = base
-        out[t.name] = base.as_strided(t.shape, _contiguous_strides(t.shape), t.offset // isz)
+        # as_strided counts its offset from the start of the storage, not
+        # from the start of the typed view
+        out[t.name] = base.as_strided(t.shape, _contiguous_strides(t.shape),
+                                      base.storage_offset() + t.offset // isz)
     return out
 
 

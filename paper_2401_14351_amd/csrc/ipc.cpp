@@ -120,11 +120,25 @@ extern "C" int32_t sllm_import_open(const sllm_ipc_desc* desc, void* stream, voi
             e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), im->ev, 0);
         }
     }
+    int32_t code = SLLM_E_HIP;
+    if (e == hipSuccess) {
+        // the descriptor comes from another process: its range must lie in
+        // the allocation the handle mapped, or views past it would fault
+        hipDeviceptr_t base = nullptr;
+        size_t size = 0;
+        what = "hipMemGetAddressRange";
+        e = hipMemGetAddressRange(&base, &size, im->base);
+        if (e == hipSuccess && (desc->bytes > size || desc->offset > size - desc->bytes)) {
+            code = SLLM_E_INVAL;
+            what = "the descriptor's range runs past the shared allocation";
+            e = hipErrorInvalidValue;
+        }
+    }
     if (e != hipSuccess) {
         if (im->ev) (void)hipEventDestroy(im->ev);
         if (im->base) (void)hipIpcCloseMemHandle(im->base);
         delete im;
-        return fail(SLLM_E_HIP, "%s: %s", what, hipGetErrorString(e));
+        return fail(code, "%s: %s", what, hipGetErrorString(e));
     }
     *dev_ptr = static_cast<uint8_t*>(im->base) + desc->offset;
     *out = im;

@@ -146,8 +146,11 @@ int32_t check_device_range(const void* p, uint64_t bytes, int device, const char
     void* base = nullptr;
     size_t size = 0;
     if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess || !base) {
-        (void)hipGetLastError();  // no range known (e.g. managed memory): nothing more to check
-        return SLLM_OK;
+        // no allocation range known (e.g. managed memory): the call cannot
+        // show that the whole range is inside one allocation, so refuse it
+        (void)hipGetLastError();
+        return fail(SLLM_E_INVAL, "%s %p: the runtime reports no allocation range for it; pass memory from hipMalloc",
+                    what, p);
     }
     const uint64_t off = (uint64_t)(static_cast<const uint8_t*>(p) - static_cast<const uint8_t*>(base));
     if (off + bytes > size)
@@ -211,16 +214,14 @@ int32_t load_cached(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     }
     SLLM_TRY(ensure_streams(h));
     SLLM_TRY(fork_streams(h, user));
-    // merge chunks that are adjacent in host memory into one copy; with a
-    // device layout a merged run goes to this stream's HBM staging chunk and
-    // one scatter launch repacks it
+    // merge chunks that follow each other in one pinned arena into one copy;
+    // with a device layout a merged run goes to this stream's HBM staging
+    // chunk and one scatter launch repacks it
     const uint64_t max_copy = h->dev_align ? h->layout.staging_stride : std::max(sdma_max_copy(), C);
     uint64_t issued = 0;
     for (uint64_t k = 0; k < n;) {
         uint64_t j = k + 1;
-        while (j < n && p->stride == C && p->host[e->chunks[j]] == p->host[e->chunks[j - 1]] + C &&
-               (j + 1 - k) * C <= max_copy)
-            ++j;
+        while (j < n && pool_follows(p, e->chunks[j - 1], e->chunks[j]) && (j + 1 - k) * C <= max_copy) ++j;
         const uint64_t x0 = k * C, x1 = std::min(j * C, T);
         const uint32_t si = (uint32_t)(issued % h->streams.size());
         hipStream_t s = h->streams[si];
@@ -270,8 +271,8 @@ void adopt_kept(sllm_ckpt* h) {
 // seq mod S: the kernel engine moves the batch in one batched gather (file
 // layout) or one K1-scatter launch per run of consecutive chunks (device
 // layout); the copy engines take one copy per run of consecutive chunks
-// whose slots are adjacent in host memory (slots are handed out in order, so
-// runs are common), or, with a device layout, one chunk per batch through
+// whose slots follow each other in one pinned arena (slots are handed out
+// in order, so runs are common), or, with a device layout, one chunk per batch through
 // the stream's HBM staging chunk and K2.  The event of the batch's first
 // slot, recorded after its work on the same stream, ends the batch.
 class GpuSink final : public BatchSink {
@@ -296,7 +297,7 @@ class GpuSink final : public BatchSink {
             for (uint32_t b0 = 0; b0 < n;) {
                 uint32_t b1 = b0 + 1;
                 while (b1 < n && b[b1].chunk == b[b1 - 1].chunk + 1 &&
-                       h_->slots[b[b1].slot].host == h_->slots[b[b1 - 1].slot].host + C)
+                       pool_follows(h_->pool, h_->slots[b[b1 - 1].slot].id, h_->slots[b[b1].slot].id))
                     ++b1;
                 const uint64_t x0 = b[b0].chunk * C, x1 = std::min(b[b1 - 1].chunk * C + C, T);
                 ++calls;

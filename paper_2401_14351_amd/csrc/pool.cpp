@@ -222,6 +222,7 @@ extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int3
     const uint64_t per_arena = std::max<uint64_t>(1, arena_target_bytes() / stride);
     p->host.reserve(n_chunks);
     p->mapped.reserve(n_chunks);
+    p->arena_of.reserve(n_chunks);
     for (uint64_t done = 0; done < n_chunks;) {
         const uint64_t k = std::min(per_arena, n_chunks - done);
         void* h = nullptr;
@@ -240,6 +241,7 @@ extern "C" int32_t sllm_pool_create(uint64_t chunk_size, uint64_t n_chunks, int3
         for (uint64_t i = 0; i < k; ++i) {
             p->host.push_back(static_cast<uint8_t*>(h) + i * stride);
             p->mapped.push_back(static_cast<const uint8_t*>(d) + i * stride);
+            p->arena_of.push_back((uint32_t)(p->arenas.size() - 1));
         }
         done += k;
     }

@@ -34,6 +34,7 @@ struct sllm_pool {
     std::vector<void*> arenas;            // pinned allocations
     std::vector<uint8_t*> host;           // per chunk: host address
     std::vector<const uint8_t*> mapped;   // per chunk: device-visible address
+    std::vector<uint32_t> arena_of;       // per chunk: index of the arena holding it
     std::vector<uint32_t> free_ids;
     std::vector<std::unique_ptr<sllm::CacheEntry>> cache;
     int users = 0;                        // open handles attached to the pool
@@ -41,6 +42,13 @@ struct sllm_pool {
 };
 
 namespace sllm {
+
+// Chunk b's bytes follow chunk a's in one pinned allocation, so one copy can
+// read both.  Two arenas may happen to sit back to back in the address
+// space, but a copy must not run from one allocation into another.
+inline bool pool_follows(const sllm_pool* p, uint32_t a, uint32_t b) {
+    return p->stride == p->chunk && p->arena_of[a] == p->arena_of[b] && p->host[b] == p->host[a] + p->chunk;
+}
 
 // Take n free chunks (NOMEM if fewer are free) / give them back.
 int32_t pool_take(sllm_pool* p, uint64_t n, std::vector<uint32_t>* out);

@@ -248,7 +248,12 @@ def _bits_of(values_f32: np.ndarray, dtype: str) -> np.ndarray:
     raise ValueError(dtype)
 
 
-def _block(spec: CheckpointSpec, i: int, t: TensorSpec, b: int, out: np.ndarray) -> None:
+def block_size(t: TensorSpec) -> int:
+    """Bytes of one generation block of ``t`` (the last block may be shorter)."""
+    return BLOCK * ITEMSIZE[t.dtype]
+
+
+def fill_block(spec: CheckpointSpec, i: int, t: TensorSpec, b: int, out: np.ndarray) -> None:
     """Fill ``out`` (uint8 bytes of element block b of tensor i)."""
     isz = ITEMSIZE[t.dtype]
     n_el = out.size // isz
@@ -273,13 +278,13 @@ def tensor_bytes(spec: CheckpointSpec, i: int, pool: Optional[ThreadPoolExecutor
     """Raw little-endian bytes of tensor ``i`` as a fresh uint8 array."""
     t = spec.tensors[i]
     out = np.empty(t.nbytes, dtype=np.uint8)
-    step = BLOCK * ITEMSIZE[t.dtype]
+    step = block_size(t)
     jobs = [(b, out[b * step:(b + 1) * step]) for b in range((t.nbytes + step - 1) // step)]
     if pool is None or len(jobs) <= 1:
         for b, o in jobs:
-            _block(spec, i, t, b, o)
+            fill_block(spec, i, t, b, o)
     else:
-        list(pool.map(lambda job: _block(spec, i, t, job[0], job[1]), jobs))
+        list(pool.map(lambda job: fill_block(spec, i, t, job[0], job[1]), jobs))
     return out
 
 

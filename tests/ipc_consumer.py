@@ -34,6 +34,19 @@ def main() -> int:
             return 1
     del views, buf
     imp.close()
+    # a descriptor whose range runs past the shared allocation is refused
+    # before anything could read it
+    bad = binding.IpcDesc.from_buffer_copy(bytes.fromhex(desc_hex))
+    bad.offset = bad.offset + bad.bytes
+    try:
+        binding.Import(bytes(bad), stream)
+    except binding.SllmError as e:
+        if e.code != -1:
+            print(f"[ipc-consumer] an out-of-range descriptor gave {e}", flush=True)
+            return 1
+    else:
+        print("[ipc-consumer] an out-of-range descriptor was accepted", flush=True)
+        return 1
     print(f"ipc ok {len(tensors)} tensors", flush=True)
     return 0
 

@@ -58,3 +58,46 @@ def test_contiguous_strides():
     assert binding._contiguous_strides((3, 5)) == (5, 1)
     assert binding._contiguous_strides((2, 0, 4)) == (4, 4, 1)
     assert binding._contiguous_strides((7,)) == (1,)
+
+
+@pytest.mark.parametrize("start", [16, 4096 + 48, 3])
+def test_views_of_a_sliced_buffer(L, tmp_path, start):
+    """The buffer is a slice that starts inside a larger allocation (a region
+    of a preallocated arena): every view still sits at buf + offset and holds
+    the tensor's bytes, not bytes from before the slice."""
+    spec = synth.tiny(33, n=30, alignment=16, max_bytes=3000)
+    tensors = [(t.name, t.dtype, t.shape, d) for t, d in zip(spec.tensors, synth.materialize(spec))]
+    binding.convert(iter(tensors), str(tmp_path), 16, 4096)
+    index = oracle.make_index(tensors, 16, 4096)
+    image = bytes(oracle.partition_bytes(tensors, 16)[:index.total_bytes])
+    arena = torch.full((start + len(image) + 64,), 0xEE, dtype=torch.uint8)
+    arena[start:start + len(image)] = torch.frombuffer(bytearray(image), dtype=torch.uint8)
+    buf = arena[start:start + len(image)]
+    with binding.Checkpoint(str(tmp_path), index_only=True) as ck:
+        entries = ck.tensors()
+    views = binding.views(buf, entries)
+    for (name, dt, shape, data), e in zip(tensors, entries):
+        v = views[name]
+        if e.nbytes:
+            assert v.data_ptr() == buf.data_ptr() + e.offset, name
+        raw = v.contiguous().reshape(-1).view(torch.uint8).numpy().tobytes()
+        assert raw == np.asarray(data).tobytes(), name
+        isz = torch.tensor([], dtype=TORCH_DTYPE[dt]).element_size()
+        if start % isz == 0 and e.offset % isz == 0:
+            assert v.dtype == TORCH_DTYPE[dt] and tuple(v.shape) == tuple(shape), name
+        else:  # the slice starts off the element alignment: raw bytes
+            assert v.dtype == torch.uint8 and v.numel() == e.nbytes, name
+
+
+def test_buffers_must_be_flat_bytes(L, tmp_path):
+    spec = synth.tiny(34, n=4, alignment=16)
+    tensors = [(t.name, t.dtype, t.shape, d) for t, d in zip(spec.tensors, synth.materialize(spec))]
+    binding.convert(iter(tensors), str(tmp_path), 16, 4096)
+    with binding.Checkpoint(str(tmp_path), index_only=True) as ck:
+        entries = ck.tensors()
+        for bad in (torch.zeros(64, dtype=torch.float32), torch.zeros(8, 8, dtype=torch.uint8),
+                    torch.zeros(128, dtype=torch.uint8)[::2]):
+            with pytest.raises(ValueError):
+                binding.views(bad, entries)
+            with pytest.raises(ValueError):
+                ck.load_into(bad)
