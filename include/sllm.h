@@ -248,6 +248,34 @@ int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream)
 int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes,
                     void* dst_dev, uint64_t dst_bytes, void* stream);
 
+/* sllm_repack for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same result, byte for byte, with no hipMalloc, hipFree or other
+ * allocation.  Its device tables (sizes, file and device offsets, and the
+ * repack plan for one window of the destination at a time) live in a fixed
+ * library area of SLLM_NOALLOC_SCRATCH_BYTES per device, which each device
+ * holds from the library's first kernel launch on it until the process
+ * ends.  The sizes travel as kernel arguments; every table is rewritten by
+ * each call, so nothing carries over between calls.
+ *   h              any open handle, INDEX_ONLY included (its index gives the
+ *                  layout); it may have been opened without a dev_alignment
+ *   dev_alignment  A2, a power of two >= 16; 0 means the handle's own
+ *   src_dev        the file-layout image, T = sllm_total_bytes of an
+ *                  unaligned handle; src_bytes >= T
+ *   dst_dev        receives T2 = sum align_up(s_i, A2) bytes; dst_bytes >= T2
+ * Buffers are device memory of the handle's device, 16-byte aligned, and do
+ * not overlap.  Enqueued on `stream`; the call returns without waiting.
+ * Calls that overlap on one device (different streams or threads, or one
+ * stream while another call's kernels still run elsewhere) race for the
+ * area: order them, for example on one stream.
+ * Errors: INVAL (no or bad alignment, overlap, a buffer that is not device
+ * memory of the handle's device), RANGE (a buffer too small, or more than
+ * SLLM_NOALLOC_MAX_TENSORS tensors), HIP. */
+#define SLLM_NOALLOC_SCRATCH_BYTES (16ull << 20)
+#define SLLM_NOALLOC_MAX_TENSORS   65536ull
+int32_t sllm_repack_noalloc(const sllm_ckpt* h, uint64_t dev_alignment, const void* src_dev,
+                            uint64_t src_bytes, void* dst_dev, uint64_t dst_bytes, void* stream);
+
 /* One tensor of the index.  `offset` is relative to the device buffer:
  * the file offset o_i, or d_i when the handle has a dev_alignment.  `name`
  * stays valid until sllm_close. */

@@ -102,6 +102,8 @@ SIGNATURES = {
     "sllm_total_bytes": (C.c_uint64, [C.c_void_p]),
     "sllm_load": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p]),
     "sllm_repack": (C.c_int32, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64, C.c_void_p]),
+    "sllm_repack_noalloc": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64,
+                                        C.c_void_p]),
     "sllm_tensor_index": (C.c_int32, [C.c_void_p, C.POINTER(TensorInfo), C.c_uint64, C.POINTER(C.c_uint64)]),
     "sllm_tensor_find": (C.c_int32, [C.c_void_p, C.c_char_p, C.POINTER(TensorInfo)]),
     "sllm_get_stats": (C.c_int32, [C.c_void_p, C.POINTER(Stats)]),
@@ -398,6 +400,14 @@ class Checkpoint:
         _check_buffer(dst)
         check(lib().sllm_repack(self._h, src.data_ptr(), src.numel(), dst.data_ptr(), dst.numel(),
                                 _stream_ptr(stream)))
+
+    def repack_noalloc(self, src, dst, dev_alignment: int = 0, stream=None) -> None:
+        """sllm_repack_noalloc: the repack into alignment ``dev_alignment``
+        (0: the handle's) with no device allocation."""
+        _check_buffer(src)
+        _check_buffer(dst)
+        check(lib().sllm_repack_noalloc(self._h, dev_alignment, src.data_ptr(), src.numel(), dst.data_ptr(),
+                                        dst.numel(), _stream_ptr(stream)))
 
     def stats(self) -> Dict[str, float]:
         s = Stats()

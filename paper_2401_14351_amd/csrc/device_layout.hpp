@@ -16,6 +16,8 @@
 #include <cstdint>
 #include <vector>
 
+#include "format.hpp"
+
 namespace sllm {
 
 struct DeviceLayout {
@@ -71,5 +73,26 @@ constexpr uint32_t kScatterBatch = 64;
 // device image (the window [k0 C, min((k0 + m) C, T))).
 int32_t launch_scatter_run(const DeviceLayout& l, uint8_t* dst, const uint8_t* const* srcs, uint64_t k0, uint32_t m,
                            uint64_t chunk, hipStream_t stream);
+
+// The allocation-free repack works in a fixed device area of
+// kNoAllocScratchBytes per device: the sizes s_i, the file offsets o_i and the
+// device offsets d_i (n + 1 entries each for the two scans) of at most
+// kNoAllocMaxTensors tensors, then K2's plan for one window of the device
+// image (kNoAllocPlanEntries blocks of kPlanBytes, 28 GiB).
+constexpr uint64_t kNoAllocScratchBytes = SLLM_NOALLOC_SCRATCH_BYTES;
+constexpr uint64_t kNoAllocMaxTensors = SLLM_NOALLOC_MAX_TENSORS;
+constexpr uint64_t kNoAllocSizeOffset = 0;
+constexpr uint64_t kNoAllocFileOffset = kNoAllocSizeOffset + 8 * kNoAllocMaxTensors;
+constexpr uint64_t kNoAllocDevOffset = kNoAllocFileOffset + 8 * (kNoAllocMaxTensors + 1);
+constexpr uint64_t kNoAllocPlanOffset = 2ull << 20;
+constexpr uint64_t kNoAllocPlanEntries = (kNoAllocScratchBytes - kNoAllocPlanOffset) / sizeof(int64_t);
+static_assert(kNoAllocDevOffset + 8 * (kNoAllocMaxTensors + 1) <= kNoAllocPlanOffset, "tables fit before the plan");
+
+// Repack the file-layout image at src (T = ix.total bytes) into dst (T2 =
+// dev_total bytes at alignment dev_align) with every device table in the
+// scratch area: no allocation.  Calls that overlap on one device race for
+// that area.  The current device must be `device`.
+int32_t repack_noalloc(const IndexData& ix, int device, uint64_t dev_align, uint64_t dev_total, const uint8_t* src,
+                       uint8_t* dst, hipStream_t stream);
 
 }  // namespace sllm

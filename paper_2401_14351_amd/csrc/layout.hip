@@ -24,6 +24,7 @@
 
 #include <algorithm>
 #include <cstdlib>
+#include <mutex>
 
 #include "common.hpp"
 #include "device_layout.hpp"
@@ -108,6 +109,7 @@ struct ScatterArgs {
     const uint8_t* run_src[kScatterBatch];
     uint64_t total;        // T
     uint32_t vec_ok;       // 16-byte aligned source vectors are addressable as such
+    uint64_t plan0;        // K2: plan entry of destination block p is shift[p - plan0]
 };
 
 // Where a launch's source bytes are: one contiguous window, a device table
@@ -343,7 +345,7 @@ __global__ __launch_bounds__(kK2Lanes) void k2_tiles(ScatterArgs a, const int64_
     __shared__ Staging stg;
     const uint64_t t = a.tile0 + blockIdx.x;
     const uint64_t yt = t * kTileBytes;
-    const int64_t sh = shift[yt / kPlanBytes];
+    const int64_t sh = shift[yt / kPlanBytes - a.plan0];
     if (sh != kMixedTile && yt >= a.y0 && yt + kTileBytes <= a.y1) {
         const uint64_t xs = yt + (uint64_t)sh;  // source of the tile's first byte
         // aligned 16-byte source vectors spanning [xs, xs + S)
@@ -365,14 +367,15 @@ __global__ __launch_bounds__(kK2Lanes) void k2_tiles(ScatterArgs a, const int64_
     scatter_span<kK2Lanes, U, NT, kWindow>(a, stg, blockIdx.x, blockIdx.x + 1);
 }
 
-// K2's plan: shift[p] = o_m - d_m when destination block p (kPlanBytes)
-// lies inside the data bytes of tensor m, else kMixedTile.
+// K2's plan for destination blocks p0 .. p0 + n_blocks - 1: shift[p - p0] =
+// o_m - d_m when block p (kPlanBytes) lies inside the data bytes of tensor
+// m, else kMixedTile.
 __global__ __launch_bounds__(256) void k3_tile_shift(const uint64_t* __restrict__ dev, const uint64_t* __restrict__ off,
-                                                     const uint64_t* __restrict__ size, uint64_t n, uint64_t n_blocks,
-                                                     int64_t* __restrict__ shift) {
+                                                     const uint64_t* __restrict__ size, uint64_t n, uint64_t p0,
+                                                     uint64_t n_blocks, int64_t* __restrict__ shift) {
     const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
     for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_blocks; p += stride) {
-        const uint64_t y = p * kPlanBytes;
+        const uint64_t y = (p0 + p) * kPlanBytes;
         const uint64_t m = owner_global(dev, 0, n - 1, y);  // d_0 = 0 <= y
         shift[p] = y + kPlanBytes <= dev[m] + size[m] ? (int64_t)(off[m] - dev[m]) : kMixedTile;
     }
@@ -473,8 +476,8 @@ int32_t device_layout_build(const std::vector<uint64_t>& file_off, const std::ve
     if (l.n_shift) {
         SLLM_HIP(hipMalloc(reinterpret_cast<void**>(&l.d_shift), l.n_shift * sizeof(int64_t)));
         const uint64_t blocks = std::min<uint64_t>(ceil_div(l.n_shift, 256), 4096);
-        k3_tile_shift<<<dim3((uint32_t)blocks), dim3(256), 0, nullptr>>>(l.d_dev, l.d_off, l.d_size, l.n, l.n_shift,
-                                                                         l.d_shift);
+        k3_tile_shift<<<dim3((uint32_t)blocks), dim3(256), 0, nullptr>>>(l.d_dev, l.d_off, l.d_size, l.n, 0,
+                                                                         l.n_shift, l.d_shift);
         SLLM_HIP(hipGetLastError());
     }
     std::vector<uint64_t> got(l.n + 1);
@@ -540,6 +543,122 @@ int32_t launch_scatter_table(const DeviceLayout& l, uint8_t* dst, const uint8_t*
     a.y0 = 0;
     a.y1 = l.dev_total;
     return launch(l, a, /*src_is_host=*/true, stream);
+}
+
+}  // namespace sllm
+
+// ---------------------------------------------------------------------------
+// Allocation-free repack
+// ---------------------------------------------------------------------------
+
+// The device memory of the allocation-free repack: the size table, the two
+// scanned offset tables and one window of K2's plan (layout in
+// device_layout.hpp).  Every device holds its own copy from the library's
+// first kernel launch on it until the process ends.  Host code reaches a
+// device's copy only through the address hipGetSymbolAddress returns with
+// that device current; the name itself is not a device address on the host.
+static __device__ __align__(256) uint8_t scratch[sllm::kNoAllocScratchBytes];
+
+namespace sllm {
+
+namespace {
+
+// Tensor sizes travel to the device as kernel arguments, kSizeBatch a launch.
+constexpr uint32_t kSizeBatch = 256;
+struct SizeBatch {
+    uint64_t* dst;
+    uint32_t m;
+    uint64_t s[kSizeBatch];
+};
+
+__global__ __launch_bounds__(kSizeBatch) void k_put_sizes(SizeBatch b) {
+    if (threadIdx.x < b.m) b.dst[threadIdx.x] = b.s[threadIdx.x];
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch[kMaxDevices] = {};
+
+// The scratch area's address on `device`, looked up once per device (the
+// caller has made `device` current).
+int32_t scratch_of(int device, uint8_t** out) {
+    if (device < 0 || device >= kMaxDevices) return fail(SLLM_E_INVAL, "device %d is out of range", device);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch[device]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(SLLM_E_HIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", device, hipGetErrorString(e));
+        g_scratch[device] = static_cast<uint8_t*>(p);
+    }
+    *out = g_scratch[device];
+    return SLLM_OK;
+}
+
+}  // namespace
+
+int32_t repack_noalloc(const IndexData& ix, int device, uint64_t dev_align, uint64_t dev_total, const uint8_t* src,
+                       uint8_t* dst, hipStream_t stream) {
+    const uint64_t n = ix.tensors.size();
+    if (n > kNoAllocMaxTensors)
+        return fail(SLLM_E_RANGE, "%llu tensors exceed the %llu of the allocation-free repack", (unsigned long long)n,
+                    (unsigned long long)kNoAllocMaxTensors);
+    if (n == 0 || dev_total == 0) return SLLM_OK;
+    uint8_t* base = nullptr;
+    SLLM_TRY(scratch_of(device, &base));
+    uint64_t* d_size = reinterpret_cast<uint64_t*>(base + kNoAllocSizeOffset);
+    uint64_t* d_off = reinterpret_cast<uint64_t*>(base + kNoAllocFileOffset);
+    uint64_t* d_dev = reinterpret_cast<uint64_t*>(base + kNoAllocDevOffset);
+    int64_t* plan = reinterpret_cast<int64_t*>(base + kNoAllocPlanOffset);
+
+    // s, then o (file layout, A) and d (device layout, A2) by the K3 scan;
+    // the index was validated against the same closed form when it was read
+    for (uint64_t i0 = 0; i0 < n; i0 += kSizeBatch) {
+        SizeBatch b{};
+        b.dst = d_size + i0;
+        b.m = (uint32_t)std::min<uint64_t>(kSizeBatch, n - i0);
+        for (uint32_t j = 0; j < b.m; ++j) b.s[j] = ix.tensors[i0 + j].nbytes;
+        k_put_sizes<<<dim3(1), dim3(kSizeBatch), 0, stream>>>(b);
+        SLLM_HIP(hipGetLastError());
+    }
+    k3_offsets_scan<<<dim3(1), dim3(1024), 0, stream>>>(d_size, n, ix.alignment, d_off);
+    SLLM_HIP(hipGetLastError());
+    k3_offsets_scan<<<dim3(1), dim3(1024), 0, stream>>>(d_size, n, dev_align, d_dev);
+    SLLM_HIP(hipGetLastError());
+
+    // windows of the device image, each planned into the plan area and then
+    // moved by K2; one stream orders each window's plan after the previous
+    // window's K2 (SLLM_NOALLOC_PLAN_BLOCKS lowers the window, to exercise
+    // several on small images)
+    DeviceLayout l;  // views of the scratch tables: owns nothing, never freed
+    l.n = n;
+    l.total = ix.total;
+    l.dev_total = dev_total;
+    l.dev_align = dev_align;
+    l.d_off = d_off;
+    l.d_size = d_size;
+    l.d_dev = d_dev;
+    l.d_shift = plan;
+    const uint64_t n_blocks = ceil_div(dev_total, kPlanBytes);
+    const uint64_t window = std::max<uint64_t>(
+        1, std::min<uint64_t>(kNoAllocPlanEntries, env_uint("SLLM_NOALLOC_PLAN_BLOCKS", (uint32_t)kNoAllocPlanEntries)));
+    for (uint64_t p0 = 0; p0 < n_blocks; p0 += window) {
+        const uint64_t nb = std::min(window, n_blocks - p0);
+        const uint64_t blocks = std::min<uint64_t>(ceil_div(nb, 256), 4096);
+        k3_tile_shift<<<dim3((uint32_t)blocks), dim3(256), 0, stream>>>(d_dev, d_off, d_size, n, p0, nb, plan);
+        SLLM_HIP(hipGetLastError());
+        ScatterArgs a{};
+        a.dst = dst;
+        a.base = src;
+        a.x0 = 0;
+        a.x1 = ix.total;
+        a.vec_ok = reinterpret_cast<uintptr_t>(src) % 16 == 0;
+        a.y0 = p0 * kPlanBytes;
+        a.y1 = std::min((p0 + nb) * kPlanBytes, dev_total);
+        a.plan0 = p0;
+        SLLM_TRY(launch(l, a, /*src_is_host=*/false, stream));
+    }
+    return SLLM_OK;
 }
 
 }  // namespace sllm

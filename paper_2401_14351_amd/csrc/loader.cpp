@@ -654,6 +654,41 @@ extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t
                                  /*src_is_host=*/false, s);
 } SLLM_CATCH_ALL
 
+extern "C" int32_t sllm_repack_noalloc(const sllm_ckpt* h, uint64_t dev_alignment, const void* src_dev,
+                                       uint64_t src_bytes, void* dst_dev, uint64_t dst_bytes, void* stream) try {
+    clear_error();
+    if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
+    const uint64_t a2 = dev_alignment ? dev_alignment : h->dev_align;
+    if (!a2) return fail(SLLM_E_INVAL, "no device alignment: pass one or open the handle with one");
+    if (!is_pow2(a2) || a2 < 16)
+        return fail(SLLM_E_INVAL, "device alignment %llu is not a power of two >= 16", (unsigned long long)a2);
+    const uint64_t n = h->ix.tensors.size();
+    if (n > kNoAllocMaxTensors)
+        return fail(SLLM_E_RANGE, "%llu tensors exceed the %llu the allocation-free repack holds", (unsigned long long)n,
+                    (unsigned long long)kNoAllocMaxTensors);
+    uint64_t t2 = 0;  // T2 = sum align_up(s_i, A2), without a host table
+    for (const TensorRec& t : h->ix.tensors) {
+        uint64_t padded = 0;
+        if (!align_up(t.nbytes, a2, &padded) || !add_ok(t2, padded, &t2))
+            return fail(SLLM_E_RANGE, "the device layout overflows 64 bits");
+    }
+    const uint64_t total = h->ix.total;
+    if (src_bytes < total || dst_bytes < t2)
+        return fail(SLLM_E_RANGE, "repack needs %llu source and %llu destination bytes", (unsigned long long)total,
+                    (unsigned long long)t2);
+    if ((reinterpret_cast<uintptr_t>(src_dev) | reinterpret_cast<uintptr_t>(dst_dev)) % 16)
+        return fail(SLLM_E_INVAL, "buffers must be 16-byte aligned");
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src_dev), d0 = reinterpret_cast<uintptr_t>(dst_dev);
+    if (total && t2 && s0 < d0 + t2 && d0 < s0 + total) return fail(SLLM_E_INVAL, "source and destination overlap");
+    if (!t2) return SLLM_OK;
+    DeviceGuard guard(h->device);
+    if (!guard.ok()) return fail(SLLM_E_HIP, "cannot make device %d current", h->device);
+    SLLM_TRY(check_device_range(src_dev, total, h->device, "source"));
+    SLLM_TRY(check_device_range(dst_dev, t2, h->device, "destination"));
+    return repack_noalloc(h->ix, h->device, a2, t2, static_cast<const uint8_t*>(src_dev), static_cast<uint8_t*>(dst_dev),
+                          static_cast<hipStream_t>(stream));
+} SLLM_CATCH_ALL
+
 namespace {
 
 void fill_info(const sllm_ckpt* h, uint32_t i, sllm_tensor_info* out) {

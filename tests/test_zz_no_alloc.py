@@ -1,0 +1,165 @@
+"""The allocation-free repack (sllm_repack_noalloc) against sllm_repack and
+the oracle, through the C ABI: two calls in a row, the second on a smaller
+checkpoint, so nothing the first call left in the library's scratch area can
+leak into the second; the destination windowed into many plan windows; the
+handle's own alignment; and the errors it reports before any device work."""
+
+import ctypes as C
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2401_14351_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = 0xC3
+
+
+def say(*a):
+    print("[gpu-noalloc]", *a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    binding.lib()  # fail loudly if the library is missing
+    return torch
+
+
+def converted(spec, d):
+    tensors = [(t.name, t.dtype, t.shape, x) for t, x in zip(spec.tensors, synth.materialize(spec))]
+    binding.convert(iter(tensors), d, spec.alignment, spec.chunk_size)
+    index = oracle.make_index(tensors, spec.alignment, 1)
+    image = bytes(oracle.partition_bytes(tensors, spec.alignment)[:index.total_bytes])
+    return tensors, index, image
+
+
+def device_bytes(torch, data: bytes, slack: int = 64):
+    return torch.frombuffer(bytearray(data + bytes(slack)), dtype=torch.uint8).to("cuda:0")
+
+
+def sentinel_buf(torch, n: int, slack: int = 64):
+    return torch.full((n + slack,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+
+
+def rc_of(h, a2, src, src_bytes, dst, dst_bytes):
+    return binding.lib().sllm_repack_noalloc(h, a2, src, src_bytes, dst, dst_bytes, None)
+
+
+def image_of(torch, buf, n):
+    torch.cuda.synchronize()
+    host = buf.cpu().numpy()
+    assert (host[n:] == SENTINEL).all(), "bytes past the image were written"
+    return host[:n].tobytes()
+
+
+def repack_both(torch, d, index, image, a2):
+    """sllm_repack (a handle opened with A2) and sllm_repack_noalloc (an
+    index-only handle, A2 passed in) of the same source, on one stream."""
+    want = bytes(oracle.repack(image, index, a2))
+    src = device_bytes(torch, image)
+    ref = sentinel_buf(torch, len(want))
+    out = sentinel_buf(torch, len(want))
+    with binding.Checkpoint(d, dev_alignment=a2) as ck:
+        assert ck.total_bytes == len(want)
+        ck.repack(src, ref)
+    with binding.Checkpoint(d, index_only=True) as ix:
+        h = ix._h
+        rc = rc_of(h, a2, src.data_ptr(), src.numel(), out.data_ptr(), out.numel())
+        assert rc == binding.SLLM_OK, binding.lib().sllm_last_error().decode()
+        got = image_of(torch, out, len(want))
+    assert image_of(torch, ref, len(want)) == want, "sllm_repack differs from the oracle"
+    if got != want:
+        a, b = np.frombuffer(got, np.uint8), np.frombuffer(want, np.uint8)
+        bad = np.nonzero(a != b)[0]
+        raise AssertionError(f"no-alloc repack A2={a2}: {bad.size} bytes differ, first at {bad[:8].tolist()}")
+    return len(want)
+
+
+def test_two_calls_then_smaller(torch_cuda, tmp_path):
+    torch = torch_cuda
+    big = synth.stress(n=600, max_bytes=1 << 20)  # 4 KiB file alignment: padding after most tensors
+    d1 = str(tmp_path / "big")
+    _, ix1, img1 = converted(big, d1)
+    say("first call: stress n=600 T", ix1.total_bytes)
+    n1 = repack_both(torch, d1, ix1, img1, 256)
+    small = synth.tiny(7, n=48, alignment=1, max_bytes=200_000)  # dense file layout: unaligned shifts
+    d2 = str(tmp_path / "small")
+    _, ix2, img2 = converted(small, d2)
+    say("second call: tiny n=48 A=1 T", ix2.total_bytes)
+    n2 = repack_both(torch, d2, ix2, img2, 16)
+    assert n2 < n1 and len(small.tensors) < len(big.tensors)
+
+
+def test_many_windows(torch_cuda, tmp_path, monkeypatch):
+    """Three plan blocks (48 KiB of destination) a window: the repack runs
+    as many plan + K2 passes through the same scratch plan area."""
+    torch = torch_cuda
+    spec = synth.stress(n=200, max_bytes=256 << 10, seed=77)
+    d = str(tmp_path / "w")
+    _, ix, img = converted(spec, d)
+    monkeypatch.setenv("SLLM_NOALLOC_PLAN_BLOCKS", "3")
+    for a2 in (4096, 256, 16):
+        say("windows of 3 plan blocks, A2", a2)
+        repack_both(torch, d, ix, img, a2)
+
+
+def test_handle_alignment(torch_cuda, tmp_path):
+    """dev_alignment = 0 takes the handle's own A2."""
+    torch = torch_cuda
+    spec = synth.tiny(11, n=40, alignment=16, max_bytes=50_000)
+    d = str(tmp_path / "h")
+    _, ix, img = converted(spec, d)
+    want = bytes(oracle.repack(img, ix, 4096))
+    src = device_bytes(torch, img)
+    out = sentinel_buf(torch, len(want))
+    with binding.Checkpoint(d, dev_alignment=4096) as ck:
+        ck.repack_noalloc(src, out)
+    assert image_of(torch, out, len(want)) == want
+
+
+def test_errors(torch_cuda, tmp_path):
+    torch = torch_cuda
+    spec = synth.tiny(3, n=12, alignment=16)
+    d = str(tmp_path / "e")
+    _, ix, img = converted(spec, d)
+    want = bytes(oracle.repack(img, ix, 256))
+    src = device_bytes(torch, img)
+    dst = sentinel_buf(torch, len(want))
+    with binding.Checkpoint(d, index_only=True) as ck:
+        h = ck._h
+        cases = [(0, len(img), len(want), -1, "no alignment"), (8, len(img), len(want), -1, "A2 < 16"),
+                 (48, len(img), len(want), -1, "A2 not a power of two"),
+                 (256, len(img) - 1, len(want), -6, "source too small"),
+                 (256, len(img), len(want) - 1, -6, "destination too small")]
+        for a2, sb, db, code, what in cases:
+            rc = rc_of(h, a2, src.data_ptr(), sb, dst.data_ptr(), db)
+            assert rc == code, (what, rc, binding.lib().sllm_last_error().decode())
+        # a host buffer is refused, not written
+        host = (C.c_uint8 * (len(want) + 64))()
+        rc = rc_of(h, 256, src.data_ptr(), len(img), C.addressof(host), len(want))
+        assert rc == -1, binding.lib().sllm_last_error().decode()
+    assert rc_of(None, 256, src.data_ptr(), len(img), dst.data_ptr(), len(want)) == -1
+    assert image_of(torch, dst, len(want)) == bytes([SENTINEL]) * len(want)
+
+
+def test_too_many_tensors(torch_cuda, tmp_path):
+    """One tensor more than the scratch area holds: RANGE, before any device work."""
+    n = 65537
+    d = str(tmp_path / "many")
+    tensors = [(f"z{i}", "i8", (0,), np.zeros(0, np.uint8)) for i in range(n)]
+    binding.convert(iter(tensors), d, 16, 1 << 20)
+    torch = torch_cuda
+    src = torch.zeros(64, dtype=torch.uint8, device="cuda:0")
+    dst = torch.zeros(64, dtype=torch.uint8, device="cuda:0")
+    with binding.Checkpoint(d, index_only=True) as ck:
+        rc = rc_of(ck._h, 256, src.data_ptr(), 64, dst.data_ptr(), 64)
+        assert rc == -6, binding.lib().sllm_last_error().decode()
+        assert b"65537" in binding.lib().sllm_last_error()
