@@ -116,20 +116,35 @@ def ensure_checkpoint(spec, d: str):
     return digests
 
 
-def measure_peaks(torch, nbytes: int = 1 << 30, reps: int = 5):
-    """Best-of-N 1 GiB pinned->HBM copy (copy engine) and HBM->HBM copy."""
+def measure_peaks(torch, nbytes: int = 1 << 30, reps: int = 5, streams=(1, 2, 4)):
+    """The pinned->HBM copy-engine peak: best of `reps` copies of `nbytes`
+    split evenly over 1, 2 and 4 streams (one hipMemcpyAsync per stream,
+    timed from a fork on the current stream to the join of them all), and
+    the best HBM->HBM copy.  Returns (best H2D GB/s, {streams: GB/s}, HBM GB/s)."""
     host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
     dev = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
     dev2 = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
     s = torch.cuda.current_stream()
+    side = [torch.cuda.Stream() for _ in range(max(streams))]
+    joins = [torch.cuda.Event() for _ in side]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    h2d = 0.0
-    for _ in range(reps):
-        e0.record(s)
-        dev.copy_(host, non_blocking=True)
-        e1.record(s)
-        e1.synchronize()
-        h2d = max(h2d, nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    by_streams = {}
+    for k in streams:
+        part = -(-nbytes // k)
+        best = 0.0
+        for _ in range(reps):
+            e0.record(s)
+            for j in range(k):
+                a, b = j * part, min(nbytes, (j + 1) * part)
+                side[j].wait_event(e0)
+                with torch.cuda.stream(side[j]):
+                    dev[a:b].copy_(host[a:b], non_blocking=True)
+                joins[j].record(side[j])
+                s.wait_event(joins[j])
+            e1.record(s)
+            e1.synchronize()
+            best = max(best, nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+        by_streams[k] = round(best, 3)
     d2d = 0.0
     for _ in range(reps):
         e0.record(s)
@@ -138,7 +153,7 @@ def measure_peaks(torch, nbytes: int = 1 << 30, reps: int = 5):
         e1.synchronize()
         d2d = max(d2d, 2 * nbytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
     del host, dev, dev2
-    return h2d, d2d
+    return max(by_streams.values()), by_streams, d2d
 
 
 def host_info():
@@ -183,6 +198,77 @@ def gpu_links():
                     "width": read("current_link_width"), "max_speed": read("max_link_speed"),
                     "max_width": read("max_link_width")})
     return out
+
+
+def pcie_function(bdf: str):
+    """Max Payload Size (set and supported), Max Read Request Size and Read
+    Completion Boundary of one PCI function, from its PCI Express capability
+    in sysfs config space; `readable` is the number of config bytes this
+    process may read (64 without privileges, too few to reach the capability)."""
+    try:
+        cfg = open(f"/sys/bus/pci/devices/{bdf}/config", "rb").read()
+    except OSError as e:
+        return {"bdf": bdf, "readable": 0, "error": str(e)}
+    out = {"bdf": bdf, "readable": len(cfg)}
+    u16 = lambda o: int.from_bytes(cfg[o:o + 2], "little")
+    u32 = lambda o: int.from_bytes(cfg[o:o + 4], "little")
+    if len(cfg) < 64 or not u16(6) & 0x10:  # no capability list
+        return out
+    ptr, seen = cfg[0x34] & 0xFC, 0
+    while ptr and ptr + 0x14 <= len(cfg) and seen < 48:
+        if cfg[ptr] == 0x10:  # PCI Express capability
+            devcap, devctl, lnkctl = u32(ptr + 4), u16(ptr + 8), u16(ptr + 0x10)
+            out.update({"mps": 128 << ((devctl >> 5) & 7), "mps_supported": 128 << (devcap & 7),
+                        "mrrs": 128 << ((devctl >> 12) & 7), "rcb": 128 if lnkctl & 0x8 else 64,
+                        "port_type": (u16(ptr + 2) >> 4) & 0xF})
+            return out
+        ptr, seen = cfg[ptr + 1] & 0xFC, seen + 1
+    return out
+
+
+def pcie_path(bdf: str):
+    """pcie_function for the GPU and every bridge above it, GPU first."""
+    try:
+        parts = os.path.realpath(f"/sys/bus/pci/devices/{bdf}").split("/")
+    except OSError:
+        return []
+    path = [c for c in parts if len(c) == 12 and c[4] == ":" and c[7] == ":" and c[10] == "."]
+    return [pcie_function(b) for b in reversed(path)]
+
+
+def tlp_ceiling(gen5_lanes_gbps: float, payload: int, overhead: int = 20) -> float:
+    """Data rate of a link carrying only completions of `payload` bytes: each
+    adds `overhead` bytes (4-byte framing token with the sequence number,
+    12-byte completion header, 4-byte LCRC) on the 128b/130b-encoded lanes.
+    Flow-control and acknowledgement packets and SKP ordered sets are not
+    counted, so the real ceiling sits a little lower."""
+    return gen5_lanes_gbps * payload / (payload + overhead)
+
+
+def pcie_ceiling():
+    """The host link's data ceiling for transfers into the GPU, derived from
+    what sysfs reports: lanes x rate after line encoding (128b/130b from
+    8 GT/s on), less the per-completion overhead at the smallest Max Payload
+    Size on the path from the root port to the GPU.  Where this process may
+    not read that far into config space, 256-byte payloads are assumed (and
+    the record says so)."""
+    links = gpu_links()
+    if not links:
+        return None
+    g = links[0]
+    try:
+        rate = float(str(g["speed"]).split()[0])
+        width = int(g["width"])
+    except (TypeError, ValueError):
+        return {"link": g}
+    encoded = rate * width * (128 / 130 if rate >= 8 else 0.8) / 8
+    path = pcie_path(g["pci"])
+    mps = [f["mps"] for f in path if "mps" in f]
+    payload = min(mps) if mps else 256
+    return {"link": f"{g['speed']} x{g['width']}", "encoded_GBps": round(encoded, 3), "path": path,
+            "payload": payload, "payload_source": "Max Payload Size on the path (config space)" if mps else
+            "assumed: config space past 64 bytes is not readable without privileges",
+            "tlp_ceiling_GBps": round(tlp_ceiling(encoded, payload), 3)}
 
 
 def cpu_baseline(d: str, budget_s: float):
@@ -307,38 +393,56 @@ def timeline_summary(path: str, T: int):
             **{k: round(statistics.mean(p[k] for p in per), 2) for k in per[0]}} if per else None
 
 
-def estimator_replay(ready, T, tiers, dram_bps, storage_bps):
-    """Feed the measured steps, in order, to the loading-time estimator
-    (q + n / b, refined from each completed load) and report how far each
-    prediction made before a step was from that step's time-to-ready."""
+def estimator_online(d, open_kw, buf, stream, T, tiers, dram_bps, storage_bps, loads: int = 10):
+    """The loading-time estimator in use (Sec. 6): before each load its time
+    is estimated (q + n / b, sllm_estimator_enqueue); the load runs on a
+    handle opened with timing; then sllm_estimator_complete_load refines b
+    from that handle's own counters (open time plus the load's device time).
+    Reports how far each estimate was from the load's time-to-ready measured
+    around open, load and synchronize."""
     est = binding.Estimator(dram_bps, storage_bps, weight=0.5)
-    err = []
-    for r in ready:
+    err, fed = [], []
+    for _ in range(loads):
         task, eta = est.enqueue(T, tiers)
-        err.append(abs(eta - r))
-        est.complete(task, r)
+        t0 = time.perf_counter()
+        with binding.Checkpoint(d, timing=True, **open_kw) as ck:
+            ck.load_into(buf, stream)
+            stream.synchronize()
+            ready = time.perf_counter() - t0
+            est.complete_load(task, ck)
+            st = ck.stats()
+        err.append(abs(eta - ready))
+        fed.append(st["open_s"] + max(st["load_s"], st["device_ms"] * 1e-3))
     tail = err[len(err) // 2:]
-    out = {"steps": len(ready), "mean_abs_err_ms": round(statistics.mean(tail) * 1e3, 3),
-           "max_abs_err_ms": round(max(tail) * 1e3, 3), "first_err_ms": round(err[0] * 1e3, 3),
+    out = {"loads": loads, "fed_from": "sllm_get_stats of each load's handle (open_s + device time)",
+           "mean_abs_err_ms": round(statistics.mean(tail) * 1e3, 3), "max_abs_err_ms": round(max(tail) * 1e3, 3),
+           "first_err_ms": round(err[0] * 1e3, 3), "mean_fed_s": round(statistics.mean(fed), 5),
            "dram_GBps": round(est.bandwidth(binding.TIER_DRAM) / 1e9, 3),
            "storage_GBps": round(est.bandwidth(binding.TIER_STORAGE) / 1e9, 3)}
     est.close()
     return out
 
 
-def ablation(torch, spec, d: str, io_threads: int = 8):
+def ablation(torch, spec, d: str, digests, io_threads: int = 8):
     """The paper's loading ladder (Sec. 7.2, performance breakdown) rebuilt on
     this machine: each rung loads the same partition file into one HBM
-    buffer, adding one technique at a time.  Rungs 1-4 are plain host code
-    (pageable buffers, torch copies), rungs 5-6 are this library."""
+    buffer and adds one technique to the rung before it.  Rungs 1-5 are
+    plain host code (torch copies), rung 6 is this library's streamed
+    pipeline.  Before each rung the buffer is filled with a sentinel; after
+    it every byte is checked against the generator's bytes."""
+    import errno
     import mmap
     import threading
+
+    import numpy as np
 
     path = os.path.join(d, "sllm.part0")
     with binding.Checkpoint(d, index_only=True) as ck:
         tensors, T = ck.tensors(), ck.total_bytes
+    offsets = [t.offset for t in tensors]
     C = spec.chunk_size
     dev = torch.empty(T, dtype=torch.uint8, device="cuda:0")
+    bounced = [False]
 
     def cold():
         fd = os.open(path, os.O_RDONLY)
@@ -346,6 +450,7 @@ def ablation(torch, spec, d: str, io_threads: int = 8):
         os.close(fd)
 
     def read_by_tensor():
+        # one read per tensor into a fresh pageable buffer, one copy per tensor
         fd = os.open(path, os.O_RDONLY)
         for t in tensors:
             b = os.pread(fd, t.nbytes, t.offset)
@@ -353,39 +458,59 @@ def ablation(torch, spec, d: str, io_threads: int = 8):
                 dev[t.offset:t.offset + t.nbytes].copy_(torch.frombuffer(bytearray(b), dtype=torch.uint8))
         os.close(fd)
 
-    def bulk(direct: bool, threads: int):
+    def chunked(direct: bool, threads: int, pinned: bool):
+        # C-byte chunk reads (a shared counter hands out chunk numbers), each
+        # copied to the GPU by the thread that read it: from a pageable
+        # buffer (the runtime stages it), or from the thread's pinned buffer
+        # (DMA straight from it).  Direct reads into pinned memory that the
+        # kernel refuses (EFAULT) land in a page-aligned bounce buffer first.
         fd = os.open(path, os.O_RDONLY | (os.O_DIRECT if direct else 0))
+        size = os.fstat(fd).st_size
         n = -(-T // C)
         counter = iter(range(n))
         lock = threading.Lock()
+        errors = []
 
         def worker():
-            buf = mmap.mmap(-1, C)  # page-aligned, pageable
-            host = torch.frombuffer(buf, dtype=torch.uint8)
-            while True:
-                with lock:
-                    k = next(counter, None)
-                if k is None:
-                    return
-                want = min(C, os.fstat(fd).st_size - k * C)
-                got = os.preadv(fd, [memoryview(buf)[:want]], k * C)
-                m = min(C, T - k * C)
-                assert got >= m
-                dev[k * C:k * C + m].copy_(host[:m])
+            try:
+                bounce = mmap.mmap(-1, C)  # page-aligned, pageable
+                host = torch.frombuffer(bounce, dtype=torch.uint8)
+                pin = torch.empty(C, dtype=torch.uint8, pin_memory=True) if pinned else None
+                pin_view = memoryview(pin.numpy()) if pinned else None
+                while True:
+                    with lock:
+                        k = next(counter, None)
+                    if k is None:
+                        return
+                    want = min(C, size - k * C)
+                    m = min(C, T - k * C)
+                    if pinned:
+                        try:
+                            got = os.preadv(fd, [pin_view[:want]], k * C)
+                        except OSError as e:
+                            if e.errno != errno.EFAULT:
+                                raise
+                            bounced[0] = True
+                            got = os.preadv(fd, [memoryview(bounce)[:want]], k * C)
+                            pin[:m].copy_(host[:m])
+                        src = pin
+                    else:
+                        got = os.preadv(fd, [memoryview(bounce)[:want]], k * C)
+                        src = host
+                    if got < m:
+                        raise OSError(f"short read of chunk {k}: {got} of {m} bytes")
+                    dev[k * C:k * C + m].copy_(src[:m])
+            except BaseException as e:  # reported by the caller
+                errors.append(e)
+
         ts = [threading.Thread(target=worker) for _ in range(threads)]
         for t in ts:
             t.start()
         for t in ts:
             t.join()
         os.close(fd)
-
-    def pinned_sequential():
-        with binding.Pool(C, -(-T // C)) as pool:
-            pool.cache(d, io_threads=io_threads, direct_io=True)
-            with binding.Checkpoint(d, pool=pool) as ck:
-                ck.load_into(dev)
-                torch.cuda.synchronize()
-            pool.evict(d)
+        if errors:
+            raise errors[0]
 
     def pipeline():
         with binding.Pool(C, 4 * io_threads) as pool:
@@ -394,13 +519,15 @@ def ablation(torch, spec, d: str, io_threads: int = 8):
                 ck.load_into(dev)
                 torch.cuda.synchronize()
 
-    rungs = [("ReadByTensor", True, read_by_tensor), ("+bulk", True, lambda: bulk(False, 1)),
-             ("+direct I/O", False, lambda: bulk(True, 1)),
-             (f"+{io_threads} I/O threads", False, lambda: bulk(True, io_threads)),
-             ("+pinned chunk pool (tiers in sequence)", False, pinned_sequential),
+    rungs = [("ReadByTensor", True, read_by_tensor),
+             ("+bulk (16 MiB chunk reads)", True, lambda: chunked(False, 1, False)),
+             ("+direct I/O", False, lambda: chunked(True, 1, False)),
+             (f"+{io_threads} I/O threads", False, lambda: chunked(True, io_threads, False)),
+             ("+pinned memory (copies from pinned chunks)", False, lambda: chunked(True, io_threads, True)),
              ("+pipeline (streamed ring)", False, pipeline)]
     out, prev = [], None
     for name, needs_cold, fn in rungs:
+        dev.fill_(0x5A)
         if needs_cold:
             cold()
         torch.cuda.synchronize()
@@ -409,11 +536,14 @@ def ablation(torch, spec, d: str, io_threads: int = 8):
         torch.cuda.synchronize()
         dt = time.perf_counter() - t0
         gbps = T / dt / 1e9
+        got = verify.check_image(torch, dev, spec, offsets, T, digests)
         out.append({"rung": name, "s": round(dt, 3), "GBps": round(gbps, 3),
-                    "step_gain": None if prev is None else round(gbps / prev, 2)})
+                    "step_gain": None if prev is None else round(gbps / prev, 2),
+                    "verified": f"every byte ({got['tensors']} tensors, {got['bytes']} bytes)"})
         prev = gbps
         log("ablation", out[-1])
-    return out
+    del dev
+    return out, {"direct_reads_into_pinned_memory": "refused (EFAULT): bounced" if bounced[0] else "accepted"}
 
 
 def thread_sweep(d: str, C: int, threads=(1, 2, 4, 8, 16)):
@@ -458,6 +588,83 @@ def block_device(path: str) -> str:
         return "unknown"
 
 
+K2_TILE = 8192    # bytes of the device image per K2 workgroup
+K2_PLAN = 16384   # bytes of the device image per entry of K2's plan
+
+
+def k2_tile_paths(file_off, dev_off, sizes, T2):
+    """How K2's tiles split between its paths for a whole-image repack: a tile
+    whose plan block lies inside one tensor's data copies straight (source
+    and destination agree mod 16) or through the byte funnel (they do not);
+    every other tile (tensor edges, padding, small tensors) takes the staged
+    general path."""
+    import numpy as np
+
+    o = np.asarray(file_off, dtype=np.int64)
+    dv = np.asarray(dev_off, dtype=np.int64)
+    s = np.asarray(sizes, dtype=np.int64)
+    blocks = np.maximum(0, (dv + s) // K2_PLAN - (-(-dv // K2_PLAN)))
+    tiles = blocks * (K2_PLAN // K2_TILE)
+    aligned = (o - dv) % 16 == 0
+    total = -(-T2 // K2_TILE)
+    straight, shifted = int(tiles[aligned].sum()), int(tiles[~aligned].sum())
+    return {"tiles": total, "straight": straight, "shifted": shifted, "general": total - straight - shifted,
+            "straight_frac": round(straight / total, 4) if total else None,
+            "shifted_frac": round(shifted / total, 4) if total else None,
+            "general_frac": round((total - straight - shifted) / total, 4) if total else None}
+
+
+def measure_k2(torch, workload: str, dev_alignment: int, stream, reps: int = 6, verify_image: bool = True):
+    """K2 on a repack that moves bytes: the workload's file-layout image,
+    loaded into HBM through a pinned ring, repacked into alignment
+    `dev_alignment` by sllm_repack `reps` times (the first untimed), each
+    timed with HIP events on the stream K2 runs on; then every byte of the
+    result is checked against the generator's bytes."""
+    spec = synth.config(workload)
+    d = os.path.join(os.environ.get("SLLM_BENCH_DIR", "/tmp/sllm_bench"), spec.name)
+    digests = ensure_checkpoint(spec, d)
+    with binding.Checkpoint(d, index_only=True) as ck:
+        T, file_off = ck.total_bytes, [t.offset for t in ck.tensors()]
+    with binding.Checkpoint(d, index_only=True, dev_alignment=dev_alignment) as ck:
+        T2, dev_off = ck.total_bytes, [t.offset for t in ck.tensors()]
+    sizes = [t.nbytes for t in spec.tensors]
+    src = torch.empty(T, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty(T2, dtype=torch.uint8, device="cuda:0")
+    slots = max(16, (1 << 30) // spec.chunk_size)
+    with binding.Pool(spec.chunk_size, slots) as ring:
+        with binding.Checkpoint(d, pool=ring, io_threads=8, ring_slots=slots) as ck:
+            ck.load_into(src, stream)
+            stream.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ms = []
+    with binding.Checkpoint(d, dev_alignment=dev_alignment, ring_slots=2, io_threads=1) as ck:
+        for i in range(reps):
+            e0.record(stream)
+            ck.repack(src, dst, stream)
+            e1.record(stream)
+            e1.synchronize()
+            if i:
+                ms.append(e0.elapsed_time(e1))
+    gbps = (T + T2) / (statistics.mean(ms) * 1e-3) / 1e9
+    summary = f"k2_tiles_repack_{workload}.md"
+    k2c = profiled_counters(summary, *K2_SOURCES)
+    out = {"workload": spec.name, "tensors": len(sizes), "alignment": spec.alignment, "dev_alignment": dev_alignment,
+           "bytes_read": T, "bytes_written": T2, "padding_written": T2 - sum(sizes),
+           "kernel_ms": round(statistics.mean(ms), 3), "kernel_ms_min": round(min(ms), 3),
+           "achieved_GBps": round(gbps, 1), "bound": "hbm", "peak": HBM_PEAK_GBPS,
+           "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+           "traffic": (k2c["fetch_bytes_per_launch"] + k2c["write_bytes_per_launch"]) if k2c else None,
+           "traffic_profile": f"profiles/{summary}" if k2c else None,
+           "tile_paths": k2_tile_paths(file_off, dev_off, sizes, T2)}
+    if verify_image:
+        t0 = time.perf_counter()
+        got = verify.check_image(torch, dst, spec, dev_off, T2, digests)
+        out["parity"] = {"checked": "every byte of the repacked image", **got, "s": round(time.perf_counter() - t0, 2)}
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def measure_extras(torch, spec, d, pool, buf, stream, engine):
     """Other engines and tiers on the same checkpoint (outside the graded step)."""
     out = {}
@@ -475,7 +682,16 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
     out[f"engine_{other}"] = {"time_to_ready_s": round(statistics.median(times), 5),
                               "GBps": round(T / statistics.median(times) / 1e9, 3)}
     log("other engine:", out[f"engine_{other}"])
-    # K2: HBM-side repack of the file-layout image into a 4 KiB-aligned device layout
+    # K2 on repacks that move bytes: the 8 GiB stress prefix (4 KiB file
+    # alignment, padding after most tensors) into A2 = 256, and the same
+    # tensors packed densely (A = 1), whose shifts need the byte funnel
+    out["repack_k2"] = measure_k2(torch, "stress-8g", 256, stream)
+    log("repack:", out["repack_k2"])
+    out["repack_k2_dense"] = measure_k2(torch, "stress-8g-dense", 256, stream)
+    log("repack (dense file):", out["repack_k2_dense"])
+    # the 7B image into A2 = 4 KiB: every 7B tensor is a multiple of 8 KiB,
+    # so that layout equals the file layout and K2 only copies (an upper
+    # bound, every tile straight)
     with binding.Checkpoint(d, pool=pool, dev_alignment=4096) as ck:
         T2 = ck.total_bytes
         dst = torch.empty(T2, dtype=torch.uint8, device="cuda:0")
@@ -490,12 +706,14 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
                 ms.append(e0.elapsed_time(e1))
         k2 = (T + T2) / (statistics.mean(ms) * 1e-3) / 1e9
         k2c = profiled_counters("k2_tiles_repack_llama-2-7b.md", *K2_SOURCES)
-        out["repack_k2"] = {"dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
-                            "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1),
-                            "bound": "hbm", "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),
-                            "traffic": (k2c["fetch_bytes_per_launch"] + k2c["write_bytes_per_launch"]) if k2c else None}
+        out["repack_k2_identity_copy"] = {
+            "workload": spec.name, "dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
+            "note": "identity layout (every tensor a multiple of 8 KiB): a copy, not a relocation",
+            "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1), "bound": "hbm",
+            "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),
+            "traffic": (k2c["fetch_bytes_per_launch"] + k2c["write_bytes_per_launch"]) if k2c else None}
         del dst
-    log("repack:", out["repack_k2"])
+    log("repack (identity copy):", out["repack_k2_identity_copy"])
     # streamed from the file with direct I/O through a 1 GiB ring, 16 readers
     # (cold: O_DIRECT bypasses the page cache), next to the storage device's
     # own peak measured the way the paper normalizes storage bandwidth
@@ -561,12 +779,24 @@ def measure_extras(torch, spec, d, pool, buf, stream, engine):
     return out
 
 
+def calibration_copy(torch):
+    """One 1 GiB HBM -> HBM copy: the kernel whose counter readings scale
+    FETCH_SIZE and WRITE_SIZE to bytes."""
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0")
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    log("calibration copy: 1 GiB HBM -> HBM")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama-2-7b", choices=list(synth.WORKLOADS) + ["stress-8g", "lora-70b-r32"])
+    ap.add_argument("--workload", default="llama-2-7b",
+                    choices=list(synth.WORKLOADS) + ["stress-8g", "stress-8g-dense", "lora-70b-r32"])
     ap.add_argument("--engine", default="kernel", choices=["kernel", "sdma"])
     ap.add_argument("--regime", default="dram", choices=["dram", "ring", "direct"],
                     help="dram: partition cached in the pinned pool (graded); ring: streamed from the file "
@@ -591,6 +821,8 @@ def main():
     ap.add_argument("--trace", default=None,
                     help="streamed regimes: write the timed loads' pipeline timeline (CSV) to this file and "
                          "summarize it (tracing waits for each load's last batches)")
+    ap.add_argument("--repack-only", action="store_true",
+                    help="time and check only the HBM repack (K2) of --workload into --dev-alignment (default 256)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with one 1 GiB HBM->HBM copy (the counter calibration kernel)")
     args = ap.parse_args()
@@ -599,6 +831,17 @@ def main():
         print(f"bench.py measures one GPU: this loader has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.repack_only:
+        import torch
+
+        torch.cuda.init()
+        stream = torch.cuda.Stream()
+        k2 = measure_k2(torch, args.workload, args.dev_alignment or 256, stream, reps=args.steps + 1)
+        print(json.dumps({"repack_k2": k2}), flush=True)
+        if args.calib_copy:
+            calibration_copy(torch)
+        return
 
     spec = synth.config(args.workload)
     d = args.dir or os.path.join(os.environ.get("SLLM_BENCH_DIR", "/tmp/sllm_bench"), spec.name)
@@ -611,11 +854,14 @@ def main():
 
     torch.cuda.init()
     if args.ablation:
-        ladder = ablation(torch, spec, d, args.io_threads)
+        ladder, notes = ablation(torch, spec, d, digests, args.io_threads)
         base = ladder[0]["GBps"]
-        print(json.dumps({"ablation": ladder, "workload": spec.name, "device": block_device(d),
+        sweep = thread_sweep(d, args.chunk_size or spec.chunk_size)
+        print(json.dumps({"ablation": ladder, "workload": spec.name,
+                          "io_threads": args.io_threads, "device": block_device(d),
                           "storage_peak": storage_peak(os.path.join(d, "sllm.part0")),
-                          "total_gain": round(ladder[-1]["GBps"] / base, 2)}), flush=True)
+                          "total_gain": round(ladder[-1]["GBps"] / base, 2), **notes,
+                          "thread_sweep": sweep, "host": host_info()}), flush=True)
         return
     if args.thread_sweep:
         sweep = thread_sweep(d, args.chunk_size or spec.chunk_size)
@@ -624,8 +870,8 @@ def main():
               flush=True)
         return
     stream = torch.cuda.Stream()
-    h2d_peak, hbm_peak = (None, None) if args.no_peaks else measure_peaks(torch)
-    log(f"measured peaks: pinned->HBM copy {h2d_peak} GB/s, HBM copy {hbm_peak} GB/s")
+    h2d_peak, h2d_by_streams, hbm_peak = (None, None, None) if args.no_peaks else measure_peaks(torch)
+    log(f"measured peaks: pinned->HBM copy {h2d_peak} GB/s (by streams {h2d_by_streams}), HBM copy {hbm_peak} GB/s")
 
     C = args.chunk_size or spec.chunk_size
     if not args.ring_slots:
@@ -722,8 +968,9 @@ def main():
         storage = storage_peak(os.path.join(d, "sllm.part0"))
         extras["storage_peak"] = storage
     tiers = binding.TIER_DRAM | (0 if cached else binding.TIER_STORAGE)
-    extras["estimator"] = estimator_replay(ready, T, tiers, (h2d_peak or 50.0) * 1e9,
-                                           (storage["GBps"] if storage else 5.0) * 1e9)
+    extras["estimator"] = estimator_online(d, open_kw, buf, stream, T, tiers, (h2d_peak or 50.0) * 1e9,
+                                           (storage["GBps"] if storage else 5.0) * 1e9,
+                                           loads=10 if cached else 3)
     if tracing:
         extras["timeline"] = timeline_summary(args.trace, T)
     if not cached:
@@ -738,6 +985,7 @@ def main():
                           "reader_starved_s": round(last_stats.get("reader_starved_s", 0.0), 3),
                           "device": block_device(d)}
 
+    link = pcie_ceiling()
     kernel_ms = [a.elapsed_time(b) for a, b in zip(ev0, ev1)]
     k_avg_s = statistics.mean(kernel_ms) * 1e-3
     achieved = T / k_avg_s / 1e9
@@ -776,7 +1024,12 @@ def main():
                                 "whole load on the caller's stream (events around sllm_load)"),
                      "kernel_ms": round(statistics.mean(kernel_ms), 3),
                      "peak_measured": None if h2d_peak is None else round(h2d_peak, 3),
+                     "peak_measured_by_streams": h2d_by_streams,
                      "frac_measured": None if h2d_peak is None else round(achieved / h2d_peak, 4),
+                     "tlp_ceiling": None if not (link and "tlp_ceiling_GBps" in link) else link["tlp_ceiling_GBps"],
+                     "frac_tlp_ceiling": None if not (link and "tlp_ceiling_GBps" in link) else
+                     round(achieved / link["tlp_ceiling_GBps"], 4),
+                     "pcie": link,
                      "hbm_copy_measured": None if hbm_peak is None else round(hbm_peak, 1),
                      "link": next((f"{g['speed']} x{g['width']}" for g in gpu_links()), None)},
         "cpu_baseline": cpu,
@@ -789,12 +1042,7 @@ def main():
     pool.close()
     if args.calib_copy:
         del buf
-        a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0")
-        b = torch.empty(1 << 30, dtype=torch.uint8, device="cuda:0")
-        torch.cuda.synchronize()
-        b.copy_(a)
-        torch.cuda.synchronize()
-        log("calibration copy: 1 GiB HBM -> HBM")
+        calibration_copy(torch)
 
 
 if __name__ == "__main__":

@@ -411,6 +411,15 @@ int32_t sllm_estimator_enqueue(sllm_estimator* e, uint64_t bytes, uint32_t tiers
  * task, INVAL for seconds <= 0. */
 int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, double seconds);
 
+/* sllm_estimator_complete with the time the handle's last load took, from
+ * its own counters (sllm_get_stats): open_s plus load_s, or plus the device
+ * time of the load when the handle was opened with SLLM_OPEN_TIMING and that
+ * is longer (a load from cached chunks returns once its work is enqueued,
+ * so only the device time covers it).  With timing on, this waits for the
+ * load's device work.  Errors: INVAL (NULL argument, nothing loaded yet),
+ * NOTFOUND, HIP. */
+int32_t sllm_estimator_complete_load(sllm_estimator* e, uint64_t task, const sllm_ckpt* h);
+
 /* Current bandwidth estimate of one tier (bytes per second).  Errors: INVAL. */
 int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bytes_per_s);
 

@@ -119,6 +119,7 @@ SIGNATURES = {
     "sllm_estimator_enqueue": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_uint32, C.POINTER(C.c_uint64),
                                            C.POINTER(C.c_double)]),
     "sllm_estimator_complete": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_double]),
+    "sllm_estimator_complete_load": (C.c_int32, [C.c_void_p, C.c_uint64, C.c_void_p]),
     "sllm_estimator_bandwidth": (C.c_int32, [C.c_void_p, C.c_uint32, C.POINTER(C.c_double)]),
     "sllm_last_error": (C.c_char_p, []),
     "sllm_strerror": (C.c_char_p, [C.c_int32]),
@@ -570,6 +571,11 @@ class Estimator:
 
     def complete(self, task: int, seconds: float) -> None:
         check(lib().sllm_estimator_complete(self._h, task, seconds))
+
+    def complete_load(self, task: int, ckpt: "Checkpoint") -> None:
+        """Complete ``task`` with the time ``ckpt``'s last load took, from the
+        handle's own counters (sllm_estimator_complete_load)."""
+        check(lib().sllm_estimator_complete_load(self._h, task, ckpt._h))
 
     def bandwidth(self, tier: int) -> float:
         out = C.c_double()

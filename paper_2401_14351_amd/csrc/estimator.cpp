@@ -1,5 +1,6 @@
 // Loading-time estimator of Sec. 6: q + n / b per server, with b the
 // slowest tier's bandwidth and b refined from measured loads.  Host-only.
+#include <algorithm>
 #include <cmath>
 #include <deque>
 #include <mutex>
@@ -95,6 +96,18 @@ extern "C" int32_t sllm_estimator_complete(sllm_estimator* e, uint64_t task, dou
         return SLLM_OK;
     }
     return fail(SLLM_E_NOTFOUND, "no queued task %llu", (unsigned long long)task);
+} SLLM_CATCH_ALL
+
+extern "C" int32_t sllm_estimator_complete_load(sllm_estimator* e, uint64_t task, const sllm_ckpt* h) try {
+    clear_error();
+    if (!e || !h) return fail(SLLM_E_INVAL, "estimator and handle must be non-NULL");
+    sllm_stats st{};
+    SLLM_TRY(sllm_get_stats(h, &st));
+    if (st.bytes_loaded == 0) return fail(SLLM_E_INVAL, "the handle has not loaded anything");
+    // the host-side call covers the reads; with timing the device events
+    // cover the copies or kernels that finish after it returns
+    const double seconds = st.open_s + std::max(st.load_s, st.device_ms >= 0 ? st.device_ms * 1e-3 : 0.0);
+    return sllm_estimator_complete(e, task, seconds);
 } SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bps) try {

@@ -311,7 +311,9 @@ def materialize(spec: CheckpointSpec, threads: Optional[int] = None) -> List[np.
 
 
 def config(name: str) -> CheckpointSpec:
-    """The five benchmark workloads by name, plus the capped stress variant."""
+    """The five benchmark workloads by name, plus the capped stress variant
+    (and that variant converted densely, for repacks whose shifts are not
+    multiples of 16 bytes)."""
     if name == "opt-125m":
         return opt_125m()
     if name.startswith("llama-2-"):
@@ -320,6 +322,10 @@ def config(name: str) -> CheckpointSpec:
         return stress()
     if name == "stress-8g":
         return stress(cap_payload=8 << 30)
+    if name == "stress-8g-dense":  # the same tensors packed with no alignment (A = 1)
+        spec = stress(cap_payload=8 << 30)
+        spec.name, spec.alignment = spec.name + "-dense", 1
+        return spec
     if name == "lora-70b-r32":
         return lora("70b", 32)
     raise KeyError(name)

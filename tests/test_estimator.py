@@ -53,3 +53,19 @@ def test_errors(est):
         binding.Estimator(0, 1)
     with pytest.raises(binding.SllmError):
         binding.Estimator(1, 1, weight=0)
+
+
+def test_complete_load_needs_a_load(est, tmp_path):
+    """A handle that has loaded nothing (an index-only open) gives no
+    measurement: INVAL, and the task stays queued."""
+    import numpy as np
+
+    d = str(tmp_path / "c")
+    binding.convert(iter([("w", "f32", (4,), np.arange(4, dtype=np.float32))]), d, 256, 1 << 20)
+    task, _ = est.enqueue(10 * GB, binding.TIER_DRAM)
+    with binding.Checkpoint(d, index_only=True) as ck:
+        with pytest.raises(binding.SllmError) as e:
+            est.complete_load(task, ck)
+        assert e.value.code == -1
+    assert est.query(0, binding.TIER_DRAM) == pytest.approx(0.2)
+    est.complete(task, 0.2)
