@@ -296,3 +296,37 @@ def test_convert_reports_a_full_disk(L, tmp_path):
         binding.convert([("w", "i8", (big.size,), big)], str(tmp_path), 256, 1 << 20)
     assert ei.value.code == -2 and "write" in ei.value.message
     assert not os.path.exists(tmp_path / "sllm.index")
+
+
+def test_repack_noalloc_host_checks(L, tmp_path):
+    """sllm_repack_noalloc refuses bad arguments before any HIP call (the
+    device pointers below are never dereferenced)."""
+    spec = synth.tiny(5, n=10, alignment=16)
+    tensors = [(t.name, t.dtype, t.shape, d) for t, d in zip(spec.tensors, synth.materialize(spec))]
+    d = str(tmp_path / "c")
+    binding.convert(iter(tensors), d, 16, 64)
+    index = oracle.make_index(tensors, 16, 64)
+    T = index.total_bytes
+    T2 = oracle.device_layout(index, 256)[1]
+    src, dst = 1 << 40, 1 << 41  # 16-byte aligned, far apart
+    with binding.Checkpoint(d, index_only=True) as ck:
+        h = ck._h
+        f = L.sllm_repack_noalloc
+        assert f(None, 256, src, T, dst, T2, None) == -1
+        assert f(h, 0, src, T, dst, T2, None) == -1           # no alignment given, none on the handle
+        assert f(h, 8, src, T, dst, T2, None) == -1           # below 16
+        assert f(h, 48, src, T, dst, T2, None) == -1          # not a power of two
+        assert f(h, 256, src, T - 1, dst, T2, None) == -6     # source too small
+        assert f(h, 256, src, T, dst, T2 - 1, None) == -6     # destination too small
+        assert f(h, 256, src + 8, T, dst, T2, None) == -1     # misaligned
+        assert f(h, 256, src, T, src + 16, T2, None) == -1    # overlap
+        assert b"overlap" in L.sllm_last_error()
+    empty = str(tmp_path / "e")
+    binding.convert(iter([]), empty, 16, 64)
+    with binding.Checkpoint(empty, index_only=True) as ck:
+        assert L.sllm_repack_noalloc(ck._h, 256, src, 0, dst, 0, None) == 0  # nothing to move
+    many = str(tmp_path / "m")
+    binding.convert(iter((f"z{i}", "i8", (0,), np.zeros(0, np.uint8)) for i in range(65537)), many, 16, 64)
+    with binding.Checkpoint(many, index_only=True) as ck:
+        assert L.sllm_repack_noalloc(ck._h, 256, src, 64, dst, 64, None) == -6
+        assert b"65536" in L.sllm_last_error()
