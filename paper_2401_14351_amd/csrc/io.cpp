@@ -1,6 +1,8 @@
 #include "io.hpp"
 
 #include <fcntl.h>
+#include <immintrin.h>
+#include <sys/mman.h>
 #include <sys/stat.h>
 #include <sys/syscall.h>
 #include <unistd.h>
@@ -13,6 +15,9 @@
 
 #ifndef STATX_DIOALIGN
 #define STATX_DIOALIGN 0x00002000U
+#endif
+#ifndef MADV_POPULATE_READ
+#define MADV_POPULATE_READ 22
 #endif
 
 namespace sllm {
@@ -68,6 +73,16 @@ int32_t open_data(const std::string& path, bool want_direct, DataFile* out) {
     f.ino = (uint64_t)st.st_ino;
     f.mtime_ns = (uint64_t)st.st_mtim.tv_sec * 1000000000ull + (uint64_t)st.st_mtim.tv_nsec;
     f.dio_align = f.direct ? query_dio_align(f.fd) : 1;
+    if (!f.direct && f.size && mapped_reads()) {
+        void* m = ::mmap(nullptr, f.size, PROT_READ, MAP_SHARED, f.fd, 0);
+        if (m != MAP_FAILED) {
+            const uint64_t len = f.size;
+            f.map = std::shared_ptr<const uint8_t>(static_cast<const uint8_t*>(m),
+                                                   [len](const uint8_t* p) { ::munmap((void*)p, len); });
+        } else {
+            log_msg(1, "mmap %s failed (%s); reading with pread", path.c_str(), std::strerror(errno));
+        }
+    }
     *out = f;
     return SLLM_OK;
 }
@@ -75,9 +90,46 @@ int32_t open_data(const std::string& path, bool want_direct, DataFile* out) {
 void close_data(DataFile* f) {
     if (f->fd >= 0) ::close(f->fd);
     f->fd = -1;
+    f->map.reset();
 }
 
 namespace {
+
+// dst <- src, n bytes, with non-temporal 32-byte stores where dst is
+// aligned (the pinned chunks are page-aligned), then a store fence so the
+// bytes are globally visible before the chunk is handed on.
+__attribute__((target("avx2"))) void copy_stream_avx2(uint8_t* dst, const uint8_t* src, uint64_t n) {
+    uint64_t head = (32 - (reinterpret_cast<uintptr_t>(dst) & 31)) & 31;
+    if (head > n) head = n;
+    std::memcpy(dst, src, head);
+    dst += head;
+    src += head;
+    n -= head;
+    uint64_t i = 0;
+    for (; i + 128 <= n; i += 128) {
+        const __m256i a = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(src + i));
+        const __m256i b = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(src + i + 32));
+        const __m256i c = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(src + i + 64));
+        const __m256i d = _mm256_loadu_si256(reinterpret_cast<const __m256i*>(src + i + 96));
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(dst + i), a);
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(dst + i + 32), b);
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(dst + i + 64), c);
+        _mm256_stream_si256(reinterpret_cast<__m256i*>(dst + i + 96), d);
+    }
+    std::memcpy(dst + i, src + i, n - i);
+    _mm_sfence();
+}
+
+void copy_stream(uint8_t* dst, const uint8_t* src, uint64_t n) {
+    static const bool avx2 = __builtin_cpu_supports("avx2");
+    if (avx2) copy_stream_avx2(dst, src, n);
+    else std::memcpy(dst, src, n);
+}
+
+// Chunk copies per populate call: a populate of a whole 64 MiB chunk would
+// hold the file's page-table lock for long; 4 MiB steps keep copy and
+// populate interleaved.
+constexpr uint64_t kMapStep = 4u << 20;
 
 // 0 on success, else the errno of the failing read (-1 for end of file).
 int pread_exact(int fd, void* buf, uint64_t n, uint64_t off) {
@@ -125,6 +177,32 @@ int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const
 
 int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
                    uint64_t* bounced) {
+    if (!f.direct && f.map) {
+        if (off > f.size || n > f.size - off)
+            return fail(SLLM_E_IO, "read %s at %llu: unexpected end of file", path.c_str(), (unsigned long long)off);
+        const uintptr_t page = 4096;
+        uint8_t* d = static_cast<uint8_t*>(dst);
+        for (uint64_t done = 0; done < n;) {
+            const uint64_t k = n - done < kMapStep ? n - done : kMapStep;
+            const uint8_t* s = f.map.get() + off + done;
+            // populate the pages first: a range the file no longer covers
+            // (truncated since it was opened) fails here instead of faulting
+            const uintptr_t a0 = reinterpret_cast<uintptr_t>(s) & ~(page - 1);
+            const uintptr_t a1 = reinterpret_cast<uintptr_t>(s + k);
+            if (::madvise(reinterpret_cast<void*>(a0), a1 - a0, MADV_POPULATE_READ) != 0) {
+                // a kernel without MADV_POPULATE_READ (EINVAL) reads the rest with pread
+                if (errno == EINVAL) return pread_full(f, d + done, n - done, off + done, path);
+                return read_error(errno == EFAULT ? -1 : errno, path, off + done);
+            }
+            copy_stream(d + done, s, k);
+            // drop the page-table entries again (the pages stay in the page
+            // cache): the reader thread pays that teardown while the GPU
+            // moves earlier chunks, instead of the caller at close
+            (void)::madvise(reinterpret_cast<void*>(a0), a1 - a0, MADV_DONTNEED);
+            done += k;
+        }
+        return SLLM_OK;
+    }
     if (!f.direct) return pread_full(f, dst, n, off, path);
     if (f.direct_into_pinned->load() != 0) {
         int e = pread_exact(f.fd, dst, n, off);
@@ -151,5 +229,10 @@ int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const
 }
 
 void drop_cache(const DataFile& f) { (void)::posix_fadvise(f.fd, 0, 0, POSIX_FADV_DONTNEED); }
+
+bool mapped_reads() {
+    const char* s = std::getenv("SLLM_READ_MAPPED");
+    return s && *s == '1';
+}
 
 }  // namespace sllm

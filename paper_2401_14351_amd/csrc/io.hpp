@@ -19,6 +19,9 @@ struct DataFile {
     // whether direct reads may land in pinned chunks: -1 not yet known, 0 no
     // (the kernel cannot pin those pages for the transfer), 1 yes
     std::shared_ptr<std::atomic<int>> direct_into_pinned = std::make_shared<std::atomic<int>>(-1);
+    // buffered files only: a read-only shared mapping of the whole file, from
+    // which chunks are copied with streaming stores (see read_chunk)
+    std::shared_ptr<const uint8_t> map;
 };
 
 // Open `path` read-only; with want_direct, try O_DIRECT first and fall back
@@ -34,10 +37,18 @@ int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const
 // straight into `dst`; where the kernel refuses direct transfers into that
 // memory (EFAULT: the pages cannot be pinned for I/O), they go through a
 // 16 MiB aligned per-thread bounce buffer instead, and *bounced counts them.
+// A buffered file with a mapping has the chunk's pages populated first
+// (which reports a range past the end of the file as an I/O error instead
+// of faulting) and then copied with non-temporal stores, so the destination
+// lines are written without first being read.
 int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
                    uint64_t* bounced);
 
 // Drop the file's pages from the page cache (for cold-read measurements).
 void drop_cache(const DataFile& f);
+
+// Whether buffered files are mapped and copied with streaming stores
+// (SLLM_READ_MAPPED=1) instead of read with pread.
+bool mapped_reads();
 
 }  // namespace sllm

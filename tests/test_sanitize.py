@@ -72,3 +72,21 @@ def test_stream_pipeline_under_asan(tmp_path):
     _build_ring("g++", ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined"], exe)
     r = _run_ring(exe, {"ASAN_OPTIONS": "detect_leaks=1:abort_on_error=1", "UBSAN_OPTIONS": "print_stacktrace=1"})
     assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, r.stderr
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
+def test_chunk_reader_under_sanitizers(tmp_path):
+    """Buffered chunk reads by pread and through the file mapping with
+    streaming stores: bytes equal the file's at every destination alignment,
+    and a read past a truncation is an I/O error rather than a fault."""
+    exe = tmp_path / "io_cpu"
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", f"-I{ROOT}/include", f"-I{CSRC}",
+           os.path.join(ROOT, "tests", "native", "io_cpu.cpp"),
+           *[os.path.join(CSRC, s) for s in ("common.cpp", "io.cpp")], "-o", str(exe), "-lpthread"]
+    subprocess.run(cmd, check=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=1", UBSAN_OPTIONS="print_stacktrace=1")
+    r = subprocess.run([str(exe), str(tmp_path)], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.strip() == "ok", r.stdout
+    assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, r.stderr
