@@ -677,3 +677,37 @@ def test_open_cache_rules(torch_cuda, opt125m, tmp_path):
             assert pool.info()["cached_checkpoints"] == 1
         pool.evict(str(d2))
         assert pool.info()["free_chunks"] == n
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+def test_mapped_reader(torch_cuda, opt125m, engine, monkeypatch, tmp_path):
+    """The opt-in mapped reader (SLLM_READ_MAPPED=1: page tables populated
+    per step, streaming-store copies): streamed loads at a page-multiple and
+    an odd chunk size, the DRAM-tier fill, and a truncated file failing with
+    SLLM_E_IO and leaving the handle usable."""
+    monkeypatch.setenv("SLLM_READ_MAPPED", "1")
+    torch = torch_cuda
+    spec, tensors, d = opt125m
+    want, _ = expected(tensors, spec.alignment)
+    for C in (1 << 20, 40000):
+        with binding.Checkpoint(d, engine=engine, chunk_size=C, ring_slots=6, io_threads=3) as ck:
+            assert_same(run_load(torch, ck, len(want)), want, f"mapped streamed C={C}")
+    with binding.Pool(1 << 20, -(-len(want) // (1 << 20))) as pool:
+        pool.cache(d, io_threads=4)
+        with binding.Checkpoint(d, pool=pool, engine=engine) as ck:
+            assert_same(run_load(torch, ck, len(want)), want, "mapped fill, cached load")
+        pool.evict(d)
+    c = tmp_path / "trunc"
+    binding.convert(iter(tensors), str(c), spec.alignment, spec.chunk_size)
+    with binding.Checkpoint(str(c), engine=engine, chunk_size=1 << 20) as ck:
+        path = c / "sllm.part0"
+        full = open(path, "rb").read()
+        with open(path, "r+b") as f:
+            f.truncate(len(full) // 2)
+        buf = torch.empty(len(want), dtype=torch.uint8, device="cuda:0")
+        with pytest.raises(binding.SllmError) as ei:
+            ck.load_into(buf)
+        assert ei.value.code == -2
+        with open(path, "wb") as f:
+            f.write(full)
+        assert_same(run_load(torch, ck, len(want)), want, "mapped, after restoring the file")
