@@ -163,3 +163,48 @@ def test_too_many_tensors(torch_cuda, tmp_path):
         rc = rc_of(ck._h, 256, src.data_ptr(), 64, dst.data_ptr(), 64)
         assert rc == -6, binding.lib().sllm_last_error().decode()
         assert b"65537" in binding.lib().sllm_last_error()
+
+
+def test_captured_in_a_graph(torch_cuda, tmp_path):
+    """The allocation-free repack recorded into a HIP graph (its first call,
+    which looks up the scratch area, runs eagerly before the capture) and
+    replayed three times over three different source images, with eager
+    copies and synchronizations between the replays: every replay equals the
+    oracle's repack of the image it read."""
+    torch = torch_cuda
+    spec = synth.stress(n=120, max_bytes=256 << 10, seed=31)
+    d = str(tmp_path / "g")
+    _, ix, img = converted(spec, d)
+    a2 = 256
+    T = ix.total_bytes
+    want0 = bytes(oracle.repack(img, ix, a2))
+    src = device_bytes(torch, img)
+    out = sentinel_buf(torch, len(want0))
+    rng = np.random.default_rng(5)
+    with binding.Checkpoint(d, index_only=True) as ck:
+        h = ck._h
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):  # the eager first call: scratch lookup, same bytes
+            assert rc_of(h, a2, src.data_ptr(), src.numel(), out.data_ptr(), out.numel()) == 0
+        torch.cuda.current_stream().wait_stream(side)
+        assert image_of(torch, out, len(want0)) == want0
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            s = torch.cuda.current_stream()
+            rc = binding.lib().sllm_repack_noalloc(h, a2, src.data_ptr(), src.numel(), out.data_ptr(), out.numel(),
+                                                   C.c_void_p(s.cuda_stream))
+        assert rc == 0, binding.lib().sllm_last_error().decode()
+        for k in range(3):
+            # a new source image: random bytes in the tensors' slots, the
+            # file layout's zero padding kept (the repack reads only data bytes)
+            raw = bytearray(img)
+            for e in ix.entries:
+                raw[e.offset:e.offset + e.nbytes] = rng.integers(0, 256, e.nbytes, dtype=np.uint8).tobytes()
+            new = bytes(raw)
+            src[:T].copy_(torch.frombuffer(bytearray(new), dtype=torch.uint8))
+            out[:len(want0)].fill_(SENTINEL)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert image_of(torch, out, len(want0)) == bytes(oracle.repack(new, ix, a2)), f"replay {k}"
