@@ -1,7 +1,6 @@
 #include "format.hpp"
 
 #include <cstring>
-#include <unordered_set>
 
 namespace sllm {
 
@@ -46,6 +45,59 @@ struct Cursor {
         pos += k;
         return true;
     }
+};
+
+// 64-bit hash of a name, eight bytes at a time (multiply-xorshift mixing).
+inline uint64_t name_hash(const std::string& s) {
+    const unsigned char* p = reinterpret_cast<const unsigned char*>(s.data());
+    size_t n = s.size();
+    uint64_t h = 0x9E3779B97F4A7C15ull ^ n;
+    auto mix = [&h](uint64_t w) {
+        h ^= w * 0xBF58476D1CE4E5B9ull;
+        h = (h ^ (h >> 31)) * 0x94D049BB133111EBull;
+    };
+    for (; n >= 8; p += 8, n -= 8) {
+        uint64_t w;
+        std::memcpy(&w, p, 8);
+        mix(w);
+    }
+    uint64_t tail = 0;
+    std::memcpy(&tail, p, n);
+    mix(tail);
+    return h ^ (h >> 29);
+}
+
+// The duplicate-name check of decode_index without an allocation per name:
+// open addressing over record positions, probing by a 64-bit hash of the
+// name and comparing names only when hashes match.
+class NameSet {
+  public:
+    explicit NameSet(const std::vector<TensorRec>& recs) : recs_(recs) {
+        size_t cap = 16;
+        while (cap < 2 * recs.size()) cap <<= 1;
+        slot_.assign(cap, kEmpty);
+        hash_.resize(recs.size());
+    }
+    // false if record i's name is already in the set
+    bool insert(uint32_t i) {
+        const std::string& name = recs_[i].name;
+        const uint64_t h = name_hash(name);
+        hash_[i] = h;
+        for (size_t k = h & (slot_.size() - 1);; k = (k + 1) & (slot_.size() - 1)) {
+            const uint32_t j = slot_[k];
+            if (j == kEmpty) {
+                slot_[k] = i;
+                return true;
+            }
+            if (hash_[j] == h && recs_[j].name == name) return false;
+        }
+    }
+
+  private:
+    static constexpr uint32_t kEmpty = UINT32_MAX;
+    const std::vector<TensorRec>& recs_;
+    std::vector<uint32_t> slot_;
+    std::vector<uint64_t> hash_;
 };
 
 }  // namespace
@@ -156,8 +208,7 @@ int32_t decode_index(const void* data, size_t n, IndexData* out) {
     // each record takes at least 25 bytes, which bounds a sane count
     if (count > (n - kHeaderBytes) / 25) return fail(SLLM_E_FORMAT, "index tensor count %llu is impossible", (unsigned long long)count);
     ix.tensors.resize(count);
-    std::unordered_set<std::string> names;
-    names.reserve(count * 2);
+    NameSet names(ix.tensors);
     uint64_t padded_sum = 0;
     for (uint64_t i = 0; i < count; ++i) {
         TensorRec& t = ix.tensors[i];
@@ -181,7 +232,7 @@ int32_t decode_index(const void* data, size_t n, IndexData* out) {
             return fail(SLLM_E_FORMAT, "record '%s' truncated", t.name.c_str());
         if (check_tensor_meta(t.name.c_str(), t.dtype, t.ndim, t.shape, t.nbytes) != SLLM_OK)
             return fail(SLLM_E_FORMAT, "record '%s': %s", t.name.c_str(), sllm_last_error());
-        if (!names.insert(t.name).second) return fail(SLLM_E_FORMAT, "duplicate tensor name '%s'", t.name.c_str());
+        if (!names.insert((uint32_t)i)) return fail(SLLM_E_FORMAT, "duplicate tensor name '%s'", t.name.c_str());
         // tensors packed in order: o_i is the end of the previous padded slot
         if (t.offset != padded_sum)
             return fail(SLLM_E_FORMAT, "record '%s': offset %llu, expected %llu", t.name.c_str(),

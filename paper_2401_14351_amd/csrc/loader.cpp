@@ -16,6 +16,7 @@
 #include <cstring>
 #include <deque>
 #include <mutex>
+#include <string_view>
 #include <unordered_map>
 
 #include "device_layout.hpp"
@@ -40,7 +41,10 @@ struct Slot {
 struct sllm_ckpt {
     std::string dir, data_path;
     IndexData ix;
-    std::unordered_map<std::string, uint32_t> by_name;
+    // name -> position, built at the first lookup by name (keys view the
+    // names in ix, which never change after open)
+    mutable std::unordered_map<std::string_view, uint32_t> by_name;
+    mutable std::once_flag by_name_once;
     int device = 0;
     uint64_t chunk = 0;             // C of this handle's loads
     uint64_t dev_align = 0;         // A2, 0 for the file layout
@@ -470,8 +474,6 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
              (unsigned long long)h->file.size, (unsigned long long)h->ix.file_bytes);
         return bail(SLLM_E_FORMAT);
     }
-    h->by_name.reserve(h->ix.tensors.size() * 2);
-    for (uint32_t i = 0; i < h->ix.tensors.size(); ++i) h->by_name.emplace(h->ix.tensors[i].name, i);
 
     // device layout: the file offsets, or the closed form at A2
     const size_t nt = h->ix.tensors.size();
@@ -717,7 +719,11 @@ extern "C" int32_t sllm_tensor_index(const sllm_ckpt* h, sllm_tensor_info* out, 
 extern "C" int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_tensor_info* out) try {
     clear_error();
     if (!h || !name || !out) return fail(SLLM_E_INVAL, "handle, name and out must be non-NULL");
-    auto it = h->by_name.find(name);
+    std::call_once(h->by_name_once, [h] {
+        h->by_name.reserve(h->ix.tensors.size() * 2);
+        for (uint32_t i = 0; i < h->ix.tensors.size(); ++i) h->by_name.emplace(h->ix.tensors[i].name, i);
+    });
+    auto it = h->by_name.find(std::string_view(name));
     if (it == h->by_name.end()) return fail(SLLM_E_NOTFOUND, "no tensor named '%s'", name);
     fill_info(h, it->second, out);
     return SLLM_OK;
