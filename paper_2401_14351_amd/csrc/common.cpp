@@ -1,5 +1,7 @@
 #include "common.hpp"
 
+#include <dlfcn.h>
+
 #include <cstdio>
 #include <cstdlib>
 
@@ -38,6 +40,50 @@ void log_msg(int level, const char* fmt, ...) {
     std::vfprintf(stderr, fmt, ap);
     std::fprintf(stderr, "\n");
     va_end(ap);
+}
+
+namespace {
+
+struct Roctx {
+    int (*push)(const char*) = nullptr;
+    int (*pop)() = nullptr;
+};
+
+// resolved once: the roctx entry points, or none
+const Roctx& roctx() {
+    static const Roctx r = [] {
+        Roctx x;
+        const char* on = std::getenv("SLLM_ROCTX");
+        if (!on || *on != '1') return x;
+        for (const char* lib : {"librocprofiler-sdk-roctx.so.1", "librocprofiler-sdk-roctx.so", "libroctx64.so.4"}) {
+            void* h = dlopen(lib, RTLD_NOW | RTLD_LOCAL);
+            if (!h) continue;
+            auto push = reinterpret_cast<int (*)(const char*)>(dlsym(h, "roctxRangePushA"));
+            auto pop = reinterpret_cast<int (*)()>(dlsym(h, "roctxRangePop"));
+            if (push && pop) {
+                x.push = push;
+                x.pop = pop;
+                log_msg(1, "roctx ranges through %s", lib);
+                return x;
+            }
+            dlclose(h);
+        }
+        log_msg(1, "SLLM_ROCTX=1 but no roctx library could be loaded");
+        return x;
+    }();
+    return r;
+}
+
+}  // namespace
+
+void range_push(const char* name) {
+    const Roctx& r = roctx();
+    if (r.push) r.push(name);
+}
+
+void range_pop() {
+    const Roctx& r = roctx();
+    if (r.pop) r.pop();
 }
 
 }  // namespace sllm

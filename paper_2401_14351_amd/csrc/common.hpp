@@ -42,6 +42,20 @@ inline double now_s() {
 int log_level();
 void log_msg(int level, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
+// Named host ranges for rocprofv3's marker trace (roctx), when SLLM_ROCTX=1
+// and the ROCm roctx library can be loaded at run time; otherwise each call
+// costs one check.  Ranges nest per thread.
+void range_push(const char* name);
+void range_pop();
+
+class Range {
+  public:
+    explicit Range(const char* name) { range_push(name); }
+    ~Range() { range_pop(); }
+    Range(const Range&) = delete;
+    Range& operator=(const Range&) = delete;
+};
+
 }  // namespace sllm
 
 // Closes the function-try-block of an extern "C" entry point that returns a

@@ -429,6 +429,7 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
 }  // namespace
 
 extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out) try {
+    Range range_("sllm_open");
     clear_error();
     const double t0 = now_s();
     if (!dir || !out) return fail(SLLM_E_INVAL, "dir and out must be non-NULL");
@@ -585,6 +586,7 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
 extern "C" uint64_t sllm_total_bytes(const sllm_ckpt* h) { return h ? h->dev_total : 0; }
 
 extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, void* stream) try {
+    Range range_("sllm_load");
     clear_error();
     if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
     if (h->busy.exchange(true)) return fail(SLLM_E_BUSY, "a load is already running on this handle");
@@ -633,6 +635,7 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
 
 extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t src_bytes, void* dst_dev,
                                uint64_t dst_bytes, void* stream) try {
+    Range range_("sllm_repack");
     clear_error();
     if (!h) return fail(SLLM_E_INVAL, "handle is NULL");
     if (!h->dev_align) return fail(SLLM_E_INVAL, "the handle was opened without a device alignment");
@@ -745,6 +748,7 @@ extern "C" int32_t sllm_get_stats(const sllm_ckpt* hc, sllm_stats* out) try {
 } SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_close(sllm_ckpt* h) try {
+    Range range_("sllm_close");
     clear_error();
     if (!h) return SLLM_OK;
     if (h->busy.load()) return fail(SLLM_E_BUSY, "a load is running on this handle");

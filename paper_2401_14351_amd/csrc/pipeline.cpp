@@ -94,7 +94,9 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
             uint64_t bounced = 0;
             trace(TraceEvent::kReadBegin, k, si, thread);
             const double r0 = now_s();
+            range_push("sllm read chunk");
             const int32_t st = read(k, si, len, &bounced);
+            range_pop();
             busy_ns += (uint64_t)((now_s() - r0) * 1e9);
             if (st == SLLM_OK) trace(TraceEvent::kReadEnd, k, si, thread);
             std::lock_guard<std::mutex> g(mu);
@@ -198,7 +200,9 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         if (batch.empty()) continue;
         std::sort(batch.begin(), batch.end(), [](const ChunkSlot& a, const ChunkSlot& b) { return a.chunk < b.chunk; });
         InFlightBatch f;
+        range_push("sllm move batch");
         rc = sink.move(batch.data(), (uint32_t)batch.size(), seq, &f.token);
+        range_pop();
         // on error part of the batch may be with the sink: its slots are not
         // handed back (the load stops, drains the sink, and the next load
         // starts from a full free list)

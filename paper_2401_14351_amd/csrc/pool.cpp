@@ -281,6 +281,7 @@ extern "C" int32_t sllm_pool_query(const sllm_pool* pc, sllm_pool_info* out) try
 } SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_threads, uint32_t flags) try {
+    Range range_("sllm_pool_cache");
     clear_error();
     if (!p || !dir) return fail(SLLM_E_INVAL, "pool and dir must be non-NULL");
     if (flags & ~SLLM_OPEN_DIRECT_IO) return fail(SLLM_E_INVAL, "unknown flags 0x%x", flags);

@@ -179,6 +179,7 @@ extern "C" int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* t) try
 } SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_writer_close(sllm_writer* w) try {
+    Range range_("sllm_writer_close");
     clear_error();
     if (!w) return fail(SLLM_E_INVAL, "writer is NULL");
     int32_t st = w->error;
@@ -214,6 +215,7 @@ extern "C" void sllm_writer_abort(sllm_writer* w) {
 
 extern "C" int32_t sllm_convert(const sllm_src_tensor* tensors, uint64_t n, const char* out_dir,
                                 const sllm_convert_opts* opts) try {
+    Range range_("sllm_convert");
     clear_error();
     if (n && !tensors) return fail(SLLM_E_INVAL, "tensors is NULL");
     sllm_writer* w = nullptr;
