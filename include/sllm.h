@@ -34,6 +34,22 @@
  *     close/destroy call.
  *   - A handle may be used by one thread at a time; different handles may
  *     be used from different threads.
+ *
+ * Environment (read by the library; none is needed for normal use).
+ *   SLLM_LOG_LEVEL        0 quiet (default), 1 info, 2 debug, on stderr.
+ *   SLLM_TRACE_FILE       streamed loads append each chunk's read, move and
+ *                         done times to this CSV file.
+ *   SLLM_ROCTX=1          host stages become roctx ranges (rocprofv3
+ *                         --marker-trace); the roctx library is loaded then.
+ *   SLLM_READ_MAPPED=1    buffered files are mapped and chunks copied with
+ *                         streaming stores instead of read with pread.
+ *   SLLM_BATCH_TARGET_MB  bytes a streamed gather batch collects (64).
+ *   SLLM_SDMA_MAX_COPY_MB largest merged copy-engine copy of cached chunks (256).
+ *   SLLM_POOL_ARENA_MB    size of each pinned allocation a pool is cut from (1024).
+ *   SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT, SLLM_K2_NT, SLLM_K2_MAX_GRID,
+ *   SLLM_K2_UNROLL, SLLM_NOALLOC_PLAN_BLOCKS
+ *                         kernel launch shapes, read at every launch (for
+ *                         measurements and tests; the defaults are tuned).
  */
 #ifndef SLLM_H
 #define SLLM_H
