@@ -68,23 +68,28 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         cv_ready.notify_all();
     };
 
-    // a reader takes the next chunk number, a free slot (with keep: slot k),
-    // reads the chunk into it and queues it
+    // a reader takes a free slot (with keep: slot k) and then the next chunk
+    // number, reads the chunk into the slot and queues it.  Slots go to
+    // chunks in chunk order, so a chunk the sink waits for is always held
+    // by a reader or already queued: a sink that consumes chunks in order
+    // cannot be left waiting for a chunk with every slot held by later ones.
     auto reader = [&](uint32_t thread) {
         for (;;) {
-            const uint64_t k = next.fetch_add(1);
-            if (k >= n) return;
+            uint64_t k;
             uint32_t si;
             {
                 const double w0 = now_s();
                 std::unique_lock<std::mutex> lk(mu);
                 if (p.keep) {
                     if (stop) return;
+                    k = next.fetch_add(1);
+                    if (k >= n) return;
                     si = (uint32_t)k;
                 } else {
-                    cv_free.wait(lk, [&] { return stop || !free_q.empty(); });
+                    cv_free.wait(lk, [&] { return stop || next.load() >= n || !free_q.empty(); });
                     starved_ns += (uint64_t)((now_s() - w0) * 1e9);
-                    if (stop) return;
+                    if (stop || next.load() >= n) return;
+                    k = next.fetch_add(1);
                     si = free_q.front();
                     free_q.pop_front();
                 }
@@ -173,7 +178,7 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
             std::unique_lock<std::mutex> lk(mu);
             // readers are reading, or will start on a free slot (a chunk of
             // their own when slots are kept)
-            const bool readers_busy = reading > 0 || (p.keep ? next.load() < n : !free_q.empty());
+            const bool readers_busy = reading > 0 || (next.load() < n && (p.keep || !free_q.empty()));
             if (ready_q.empty() && !stop) {
                 if (!readers_busy && !inflight.empty())
                     wait_sink = true;  // every slot is with the sink

@@ -280,6 +280,149 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
     return 0;
 }
 
+// A sink that consumes chunks strictly in chunk order: its worker waits
+// (bounded) for chunk k to be moved before it copies chunk k and marks it
+// done.  With slots handed to chunks out of order, every slot could end up
+// holding a later chunk while the worker waits for an earlier one; the
+// bounded wait then reports it.
+class InOrderSink final : public BatchSink {
+  public:
+    InOrderSink(std::vector<uint8_t>& slots, uint64_t stride, uint32_t n_slots, std::vector<uint8_t>& dst, uint64_t C,
+                uint64_t T)
+        : slots_(slots), stride_(stride), dst_(dst), C_(C), T_(T), n_(ceil_div(T, C)), slot_of_(n_, 0),
+          done_(n_, 0), pending_(n_slots, 0), worker_([this] { run(); }) {}
+
+    ~InOrderSink() override {
+        drain();
+        worker_.join();
+    }
+
+    int32_t move(const ChunkSlot* b, uint32_t n, uint64_t, uint64_t* token) override {
+        std::lock_guard<std::mutex> g(mu_);
+        for (uint32_t i = 0; i < n; ++i) {
+            if (slot_of_[b[i].chunk] || pending_[b[i].slot]++) ++g_violations;
+            slot_of_[b[i].chunk] = b[i].slot + 1;
+        }
+        *token = b[0].chunk;
+        cv_.notify_all();
+        return SLLM_OK;
+    }
+
+    int32_t done(uint64_t k, bool block) override {
+        std::unique_lock<std::mutex> lk(mu_);
+        if (block) cv_done_.wait(lk, [&] { return done_[k] || finished_; });
+        if (done_[k]) return 1;
+        if (finished_) return fail(SLLM_E_IO, "in-order sink stopped before chunk %llu", (unsigned long long)k);
+        return 0;
+    }
+
+    void drain() override {
+        std::unique_lock<std::mutex> lk(mu_);
+        abort_ = true;
+        cv_.notify_all();
+        cv_done_.wait(lk, [&] { return finished_; });
+    }
+
+    void check_free(uint32_t si) {
+        std::lock_guard<std::mutex> g(mu_);
+        if (pending_[si]) ++g_violations;
+    }
+
+    bool timed_out() {
+        std::lock_guard<std::mutex> g(mu_);
+        return timed_out_;
+    }
+
+  private:
+    void run() {
+        for (uint64_t k = 0; k < n_; ++k) {
+            uint32_t slot;
+            {
+                std::unique_lock<std::mutex> lk(mu_);
+                const bool ok = cv_.wait_for(lk, std::chrono::seconds(5), [&] { return abort_ || slot_of_[k] != 0; });
+                if (!ok) timed_out_ = true;
+                if (!ok || abort_) break;
+                slot = slot_of_[k] - 1;
+            }
+            const uint64_t off = k * C_, len = std::min(C_, T_ - off);
+            std::memcpy(dst_.data() + off, slots_.data() + (uint64_t)slot * stride_, len);
+            {
+                std::lock_guard<std::mutex> g(mu_);
+                --pending_[slot];
+                done_[k] = 1;
+            }
+            cv_done_.notify_all();
+        }
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            finished_ = true;
+        }
+        cv_done_.notify_all();
+    }
+
+    std::vector<uint8_t>& slots_;
+    uint64_t stride_;
+    std::vector<uint8_t>& dst_;
+    uint64_t C_, T_, n_;
+    std::vector<uint32_t> slot_of_;
+    std::vector<uint8_t> done_;
+    std::vector<int> pending_;
+    std::mutex mu_;
+    std::condition_variable cv_, cv_done_;
+    bool abort_ = false, finished_ = false, timed_out_ = false;
+    std::thread worker_;
+};
+
+// Several loads through an in-order sink (a fresh one per load), with one
+// chunk per batch.
+int run_in_order_case(const Case& cs, uint64_t seed) {
+    std::mt19937_64 rng(seed);
+    const uint64_t n = ceil_div(cs.T, cs.C);
+    if (n == 0) return 0;
+    std::vector<uint8_t> file(cs.T);
+    for (auto& b : file) b = (uint8_t)rng();
+    std::vector<uint8_t> slots((uint64_t)cs.slots * cs.C);
+    std::vector<uint8_t> dst(cs.T);
+    std::mutex rng_mu;
+    for (int load = 0; load < 3; ++load) {
+        std::fill(dst.begin(), dst.end(), 0xEE);
+        InOrderSink sink(slots, cs.C, cs.slots, dst, cs.C, cs.T);
+        ChunkReader read = [&](uint64_t k, uint32_t si, uint64_t len, uint64_t*) -> int32_t {
+            uint32_t delay;
+            {
+                std::lock_guard<std::mutex> g(rng_mu);
+                delay = (uint32_t)(rng() % 200);
+            }
+            if (delay) std::this_thread::sleep_for(std::chrono::microseconds(delay));
+            sink.check_free(si);
+            std::memcpy(slots.data() + (uint64_t)si * cs.C, file.data() + k * cs.C, len);
+            return SLLM_OK;
+        };
+        StreamPlan plan;
+        plan.chunk = cs.C;
+        plan.total = cs.T;
+        plan.read_end = cs.T;
+        plan.io_threads = cs.threads;
+        plan.n_slots = cs.slots;
+        plan.max_batch = 1;
+        plan.target = 1;
+        std::deque<InFlightBatch> inflight;
+        StreamStats ss;
+        int32_t st = run_stream(plan, read, sink, inflight, &ss);
+        if (st == SLLM_OK) st = reclaim_batches(sink, inflight);
+        if (st != SLLM_OK || sink.timed_out()) {
+            std::printf("in-order load %d: status %d (%s), timed out %d\n", load, st, sllm_last_error(),
+                        (int)sink.timed_out());
+            return 1;
+        }
+        if (std::memcmp(dst.data(), file.data(), cs.T) != 0) {
+            std::printf("in-order load %d: image differs\n", load);
+            return 1;
+        }
+    }
+    return 0;
+}
+
 }  // namespace
 
 int main(int argc, char** argv) {
@@ -303,6 +446,19 @@ int main(int argc, char** argv) {
                         (unsigned long long)cs.target, (int)cs.keep, inject);
             ++failures;
             if (failures > 5) break;
+        }
+    }
+    // in-order sinks: small rings, more readers than slots, slow random reads
+    for (int i = 0; i < n_cases / 3 && failures <= 5; ++i) {
+        Case cs{};
+        cs.C = Cs[rng() % 6];
+        cs.T = 1 + rng() % (40 * cs.C);
+        cs.slots = 1 + (uint32_t)(rng() % 4);
+        cs.threads = 1 + (uint32_t)(rng() % 6);
+        if (run_in_order_case(cs, rng()) != 0) {
+            std::printf("in-order case %d failed: T=%llu C=%llu slots=%u threads=%u\n", i, (unsigned long long)cs.T,
+                        (unsigned long long)cs.C, cs.slots, cs.threads);
+            ++failures;
         }
     }
     if (g_violations.load()) {
