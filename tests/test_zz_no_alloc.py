@@ -208,3 +208,28 @@ def test_captured_in_a_graph(torch_cuda, tmp_path):
             g.replay()
             torch.cuda.synchronize()
             assert image_of(torch, out, len(want0)) == bytes(oracle.repack(new, ix, a2)), f"replay {k}"
+
+
+def test_allocates_no_device_memory(torch_cuda, tmp_path):
+    """After the first call on the device (which loads the library's code
+    object and with it the scratch area), further calls leave the device's
+    free memory exactly as it was: nothing is allocated, not even inside
+    the runtime."""
+    torch = torch_cuda
+    spec = synth.stress(n=300, max_bytes=1 << 20, seed=41)
+    d = str(tmp_path / "m")
+    _, ix, img = converted(spec, d)
+    want = bytes(oracle.repack(img, ix, 256))
+    src = device_bytes(torch, img)
+    out = sentinel_buf(torch, len(want))
+    with binding.Checkpoint(d, index_only=True) as ck:
+        h = ck._h
+        assert rc_of(h, 256, src.data_ptr(), src.numel(), out.data_ptr(), out.numel()) == 0
+        torch.cuda.synchronize()
+        free0, _ = torch.cuda.mem_get_info()
+        for _ in range(3):
+            assert rc_of(h, 256, src.data_ptr(), src.numel(), out.data_ptr(), out.numel()) == 0
+        torch.cuda.synchronize()
+        free1, _ = torch.cuda.mem_get_info()
+    assert free1 == free0, f"device free memory moved by {free0 - free1} bytes"
+    assert image_of(torch, out, len(want)) == want
