@@ -200,30 +200,35 @@ def gpu_links():
     return out
 
 
+def pcie_capability(cfg: bytes) -> dict:
+    """Max Payload Size (set and supported), Max Read Request Size, Read
+    Completion Boundary and port type from a PCI function's config space
+    bytes: the PCI Express capability (ID 0x10) found by walking the
+    capability list.  Empty when the bytes do not reach it."""
+    u16 = lambda o: int.from_bytes(cfg[o:o + 2], "little")
+    u32 = lambda o: int.from_bytes(cfg[o:o + 4], "little")
+    if len(cfg) < 64 or not u16(6) & 0x10:  # no capability list
+        return {}
+    ptr, seen = cfg[0x34] & 0xFC, 0
+    while ptr and ptr + 0x14 <= len(cfg) and seen < 48:
+        if cfg[ptr] == 0x10:
+            devcap, devctl, lnkctl = u32(ptr + 4), u16(ptr + 8), u16(ptr + 0x10)
+            return {"mps": 128 << ((devctl >> 5) & 7), "mps_supported": 128 << (devcap & 7),
+                    "mrrs": 128 << ((devctl >> 12) & 7), "rcb": 128 if lnkctl & 0x8 else 64,
+                    "port_type": (u16(ptr + 2) >> 4) & 0xF}
+        ptr, seen = cfg[ptr + 1] & 0xFC, seen + 1
+    return {}
+
+
 def pcie_function(bdf: str):
-    """Max Payload Size (set and supported), Max Read Request Size and Read
-    Completion Boundary of one PCI function, from its PCI Express capability
-    in sysfs config space; `readable` is the number of config bytes this
-    process may read (64 without privileges, too few to reach the capability)."""
+    """pcie_capability of one PCI function from sysfs; `readable` is the
+    number of config bytes this process may read (64 without privileges,
+    too few to reach the capability)."""
     try:
         cfg = open(f"/sys/bus/pci/devices/{bdf}/config", "rb").read()
     except OSError as e:
         return {"bdf": bdf, "readable": 0, "error": str(e)}
-    out = {"bdf": bdf, "readable": len(cfg)}
-    u16 = lambda o: int.from_bytes(cfg[o:o + 2], "little")
-    u32 = lambda o: int.from_bytes(cfg[o:o + 4], "little")
-    if len(cfg) < 64 or not u16(6) & 0x10:  # no capability list
-        return out
-    ptr, seen = cfg[0x34] & 0xFC, 0
-    while ptr and ptr + 0x14 <= len(cfg) and seen < 48:
-        if cfg[ptr] == 0x10:  # PCI Express capability
-            devcap, devctl, lnkctl = u32(ptr + 4), u16(ptr + 8), u16(ptr + 0x10)
-            out.update({"mps": 128 << ((devctl >> 5) & 7), "mps_supported": 128 << (devcap & 7),
-                        "mrrs": 128 << ((devctl >> 12) & 7), "rcb": 128 if lnkctl & 0x8 else 64,
-                        "port_type": (u16(ptr + 2) >> 4) & 0xF})
-            return out
-        ptr, seen = cfg[ptr + 1] & 0xFC, seen + 1
-    return out
+    return {"bdf": bdf, "readable": len(cfg), **pcie_capability(cfg)}
 
 
 def pcie_path(bdf: str):
