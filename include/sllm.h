@@ -233,7 +233,9 @@ typedef struct sllm_ckpt sllm_ckpt;
  * (defaults above, device 0).  With a dev_alignment the handle keeps device
  * tables of 24 bytes per tensor plus 8 bytes per 16 KiB of the device image
  * (the repack kernel's plan), built here.
- * Errors: INVAL, IO, FORMAT, NOMEM, HIP. */
+ * Errors: INVAL (also: direct reads where the chunk size or the padded file
+ * length F is not a multiple of the file's direct-I/O alignment), IO,
+ * FORMAT, NOMEM, HIP. */
 int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_ckpt** out);
 
 /* Bytes a load writes: T (file layout) or T2 (dev_alignment != 0); 0 for a

@@ -529,9 +529,11 @@ extern "C" int32_t sllm_open(const char* dir, const sllm_open_opts* opts, sllm_c
         }
         if (st != SLLM_OK) return bail(st);
     }
-    if (!h->cached && h->file.direct && h->chunk % h->file.dio_align) {
-        fail(SLLM_E_INVAL, "direct reads need chunk size %llu to be a multiple of %llu", (unsigned long long)h->chunk,
-             (unsigned long long)h->file.dio_align);
+    // direct reads run to the 4 KiB-padded file end, so every read's offset
+    // and length must be multiples of the file's direct-I/O alignment
+    if (!h->cached && h->file.direct && (h->chunk % h->file.dio_align || h->ix.file_bytes % h->file.dio_align)) {
+        fail(SLLM_E_INVAL, "direct reads need chunk size %llu and file size %llu to be multiples of %llu",
+             (unsigned long long)h->chunk, (unsigned long long)h->ix.file_bytes, (unsigned long long)h->file.dio_align);
         return bail(SLLM_E_INVAL);
     }
 
@@ -623,7 +625,15 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
         uint8_t* dst = static_cast<uint8_t*>(dev_dst);
         st = h->cached ? load_cached(h, dst, user) : load_streamed(h, dst, user);
     }
-    if (st != SLLM_OK) return st;
+    if (st != SLLM_OK) {
+        // a load that failed part way may have queued copies or launches
+        // before the failing call: let them finish, so that the caller may
+        // free the destination as soon as the error is returned (the copy
+        // streams are the handle's own, invisible to the caller's allocator)
+        for (hipStream_t s : h->streams) (void)hipStreamSynchronize(s);
+        (void)hipStreamSynchronize(user);
+        return st;
+    }
     if (timing) {
         SLLM_HIP(hipEventRecord(h->t1_ev, user));
         h->timed = true;

@@ -75,13 +75,12 @@ int32_t read_small_file(const std::string& path, std::string* out) {
 
 // Run fn(k) for k in [0, n) on `threads` threads; stop at the first failure
 // and return its status (with its message re-recorded on the calling thread).
-int32_t parallel_chunks(uint64_t n, uint32_t threads, int device, const std::function<int32_t(uint64_t)>& fn) {
+int32_t parallel_chunks(uint64_t n, uint32_t threads, const std::function<int32_t(uint64_t)>& fn) {
     std::atomic<uint64_t> next{0};
     std::atomic<int32_t> status{SLLM_OK};
     std::mutex mu;
     std::string msg;
     auto worker = [&] {
-        if (device >= 0) (void)hipSetDevice(device);
         for (;;) {
             if (status.load() != SLLM_OK) return;
             uint64_t k = next.fetch_add(1);
@@ -191,7 +190,7 @@ void prefault(const std::vector<void*>& arenas, uint64_t arena_bytes_last, uint6
             pieces.push_back({static_cast<uint8_t*>(arenas[a]) + o, std::min(kPiece, n - o)});
     }
     const unsigned hw = std::thread::hardware_concurrency();
-    (void)parallel_chunks(pieces.size(), std::min(16u, hw ? hw : 1u), -1, [&](uint64_t k) {
+    (void)parallel_chunks(pieces.size(), std::min(16u, hw ? hw : 1u), [&](uint64_t k) {
         volatile uint8_t* p = pieces[k].p;
         for (uint64_t o = 0; o < pieces[k].n; o += 4096) p[o] = 0;
         return SLLM_OK;
@@ -317,7 +316,7 @@ extern "C" int32_t sllm_pool_cache(sllm_pool* p, const char* dir, uint32_t io_th
     // read chunk k into its pool chunk; direct reads run to the 4 KiB-padded
     // file end so that their lengths stay block multiples
     const uint64_t read_end = f.direct ? ix.file_bytes : ix.total;
-    int32_t st = parallel_chunks(n, io_threads ? io_threads : 4, -1, [&](uint64_t k) {
+    int32_t st = parallel_chunks(n, io_threads ? io_threads : 4, [&](uint64_t k) {
         const uint64_t off = k * C;
         return read_chunk(f, p->host[ids[k]], std::min(C, read_end - off), off, data_path, nullptr);
     });

@@ -82,8 +82,7 @@ namespace sllm {
 int32_t read_small_file(const std::string& path, std::string* out);
 
 // Run fn(k) for every k in [0, n) on `threads` threads (the caller's among
-// them), stopping at the first failure; worker threads make `device`
-// current first when device >= 0.
-int32_t parallel_chunks(uint64_t n, uint32_t threads, int device, const std::function<int32_t(uint64_t)>& fn);
+// them), stopping at the first failure.
+int32_t parallel_chunks(uint64_t n, uint32_t threads, const std::function<int32_t(uint64_t)>& fn);
 
 }  // namespace sllm
