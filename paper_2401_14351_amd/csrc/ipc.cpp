@@ -35,7 +35,7 @@ extern "C" int32_t sllm_export_create(const void* dev_ptr, uint64_t bytes, int32
     if (hipMemGetAddressRange(&base, &size, const_cast<void*>(dev_ptr)) != hipSuccess || !base)
         return fail(SLLM_E_INVAL, "%p is not device memory", dev_ptr);
     const uint64_t off = (uint64_t)((const uint8_t*)dev_ptr - (const uint8_t*)base);
-    if (off + bytes > size) return fail(SLLM_E_INVAL, "range runs past its allocation");
+    if (bytes > size || off > size - bytes) return fail(SLLM_E_INVAL, "range runs past its allocation");
     if (size > SLLM_IPC_MAX_ALLOCATION)
         return fail(SLLM_E_INVAL, "allocation of %zu bytes is larger than the %llu bytes shared across processes", size,
                     (unsigned long long)SLLM_IPC_MAX_ALLOCATION);

@@ -157,7 +157,7 @@ int32_t check_device_range(const void* p, uint64_t bytes, int device, const char
                     what, p);
     }
     const uint64_t off = (uint64_t)(static_cast<const uint8_t*>(p) - static_cast<const uint8_t*>(base));
-    if (off + bytes > size)
+    if (bytes > size || off > size - bytes)
         return fail(SLLM_E_RANGE, "%s: %llu bytes from %p run past the end of its allocation", what,
                     (unsigned long long)bytes, p);
     return SLLM_OK;
