@@ -46,8 +46,8 @@
  *   SLLM_BATCH_TARGET_MB  bytes a streamed gather batch collects (64).
  *   SLLM_SDMA_MAX_COPY_MB largest merged copy-engine copy of cached chunks (256).
  *   SLLM_POOL_ARENA_MB    size of each pinned allocation a pool is cut from (1024).
- *   SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT, SLLM_K2_NT, SLLM_K2_MAX_GRID,
- *   SLLM_K2_UNROLL, SLLM_NOALLOC_PLAN_BLOCKS
+ *   SLLM_K1_BLOCKS, SLLM_K1_STREAM_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT,
+ *   SLLM_K2_NT, SLLM_K2_MAX_GRID, SLLM_K2_UNROLL, SLLM_NOALLOC_PLAN_BLOCKS
  *                         kernel launch shapes, read at every launch (for
  *                         measurements and tests; the defaults are tuned).
  */

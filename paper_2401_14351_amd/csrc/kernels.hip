@@ -123,6 +123,8 @@ GatherShape gather_shape() {
     GatherShape s;
     s.blocks = env_u32("SLLM_K1_BLOCKS", 512);
     if (s.blocks == 0) s.blocks = 1;
+    s.stream_blocks = env_u32("SLLM_K1_STREAM_BLOCKS", 64);
+    if (s.stream_blocks == 0) s.stream_blocks = 1;
     s.unroll = env_u32("SLLM_K1_UNROLL", 4);
     if (s.unroll != 1 && s.unroll != 2 && s.unroll != 4) s.unroll = 4;
     s.nontemporal = env_u32("SLLM_K1_NT", 0) != 0;
@@ -131,10 +133,11 @@ GatherShape gather_shape() {
 
 namespace {
 
-int32_t launch_tiles(GatherArgs a, uint64_t tpc, uint64_t n_chunks, const GatherShape& sh, hipStream_t stream) {
+int32_t launch_tiles(GatherArgs a, uint64_t tpc, uint64_t n_chunks, const GatherShape& sh, uint32_t blocks,
+                     hipStream_t stream) {
     a.tiles_per_chunk = (uint32_t)tpc;
     a.n_tiles = (uint32_t)(n_chunks * tpc);
-    const uint32_t grid = a.n_tiles < sh.blocks ? a.n_tiles : sh.blocks;
+    const uint32_t grid = a.n_tiles < blocks ? a.n_tiles : blocks;
     const dim3 gd(grid), bd(kThreads);
     switch (sh.unroll * 2 + (sh.nontemporal ? 1 : 0)) {
         case 2: k1_gather<1, false><<<gd, bd, 0, stream>>>(a); break;
@@ -183,7 +186,7 @@ int32_t launch_gather_batch(uint8_t* dst, const uint8_t* const* srcs, const uint
     }
     const uint64_t tpc = ceil_div(chunk, (uint64_t)kThreads * kVec * sh.unroll);
     if (tpc * n >= (1ull << 31)) return fail(SLLM_E_INVAL, "gather batch: chunk size too large");
-    return launch_tiles(a, tpc, n, sh, stream);
+    return launch_tiles(a, tpc, n, sh, sh.stream_blocks, stream);
 }
 
 int32_t launch_gather(const GatherLaunch& g, hipStream_t stream) {
@@ -210,6 +213,8 @@ int32_t launch_gather(const GatherLaunch& g, hipStream_t stream) {
     }
     const uint64_t tile = (uint64_t)kThreads * kVec * sh.unroll;
     const uint64_t tpc = ceil_div(g.chunk, tile);
+    const bool whole = g.first_chunk == 0 && g.n_chunks == ceil_div(g.total, g.chunk);
+    const uint32_t blocks = whole ? sh.blocks : sh.stream_blocks;
     // launch at most 2^31 tiles at a time
     const uint64_t max_chunks = tpc > (1ull << 31) ? 0 : (1ull << 31) / tpc;
     if (max_chunks == 0) return fail(SLLM_E_INVAL, "gather: chunk size %llu too large", (unsigned long long)g.chunk);
@@ -217,7 +222,7 @@ int32_t launch_gather(const GatherLaunch& g, hipStream_t stream) {
         const uint64_t nc = g.n_chunks - c0 < max_chunks ? g.n_chunks - c0 : max_chunks;
         a.table = g.table ? g.table + c0 : nullptr;
         a.first_chunk = g.first_chunk + c0;
-        SLLM_TRY(launch_tiles(a, tpc, nc, sh, stream));
+        SLLM_TRY(launch_tiles(a, tpc, nc, sh, blocks, stream));
     }
     return SLLM_OK;
 }

@@ -33,11 +33,16 @@ int32_t launch_gather_batch(uint8_t* dst, const uint8_t* const* srcs, const uint
                             uint64_t chunk, uint64_t total, hipStream_t stream);
 
 // Kernel launch shape knobs, read from the environment at every launch:
-// SLLM_K1_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT.
+// SLLM_K1_BLOCKS, SLLM_K1_STREAM_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT.
 struct GatherShape {
-    uint32_t blocks;   // persistent grid size
-    uint32_t unroll;   // 16-byte vectors per lane per tile: 1, 2 or 4
-    bool nontemporal;  // streaming (non-temporal) loads and stores
+    uint32_t blocks;         // persistent grid of a launch that moves the whole image
+    uint32_t stream_blocks;  // persistent grid of a launch that moves part of it
+                             // (a streamed batch, run or chunk): such launches
+                             // overlap on the copy streams, and a small grid
+                             // each keeps the reads in flight near what the
+                             // link needs
+    uint32_t unroll;         // 16-byte vectors per lane per tile: 1, 2 or 4
+    bool nontemporal;        // streaming (non-temporal) loads and stores
 };
 GatherShape gather_shape();
 

@@ -402,7 +402,8 @@ uint64_t y_of(const DeviceLayout& l, uint64_t x) {
 // Launch shape, read at every launch so that one process can compare shapes:
 // SLLM_K2_NT (streaming stores) and SLLM_K2_MAX_GRID (workgroups a launch)
 // for HBM sources; SLLM_K2_UNROLL (4 or 8 vectors per lane) and
-// SLLM_K1_BLOCKS (grid) for host sources.
+// SLLM_K1_BLOCKS / SLLM_K1_STREAM_BLOCKS (grid of a launch that moves the
+// whole image / part of it, as for K1) for host sources.
 int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream_t stream) {
     a.off = l.d_off;
     a.size = l.d_size;
@@ -434,7 +435,9 @@ int32_t launch(const DeviceLayout& l, ScatterArgs a, bool src_is_host, hipStream
     const uint64_t tile = (uint64_t)kThreads * 16 * unroll;
     a.tile0 = a.y0 / tile;
     a.n_tiles = ceil_div(a.y1, tile) - a.tile0;
-    const uint32_t want = std::max<uint32_t>(1, env_uint("SLLM_K1_BLOCKS", 512));
+    // a chunk table carries the whole image; runs and windows are parts of it
+    const uint32_t want = std::max<uint32_t>(
+        1, a.table ? env_uint("SLLM_K1_BLOCKS", 512) : env_uint("SLLM_K1_STREAM_BLOCKS", 64));
     const dim3 grid((uint32_t)std::min<uint64_t>(a.n_tiles, want)), block(kThreads);
     const bool u8 = unroll == 8;
     if (a.run_n) u8 ? k_scatter<8, false, kRun><<<grid, block, 0, stream>>>(a) : k_scatter<4, false, kRun><<<grid, block, 0, stream>>>(a);

@@ -184,7 +184,8 @@ def test_opt125m_file_layout(torch_cuda, opt125m, engine, cached):
 
 @pytest.mark.parametrize("engine", ["kernel", "sdma"])
 @pytest.mark.parametrize("shape", [{}, {"SLLM_K2_UNROLL": "4"}, {"SLLM_K2_NT": "0", "SLLM_K2_MAX_GRID": "997"},
-                                   {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1", "SLLM_K1_BLOCKS": "96"}])
+                                   {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1", "SLLM_K1_BLOCKS": "96"},
+                                   {"SLLM_K1_STREAM_BLOCKS": "3"}])
 def test_opt125m_device_layout_and_repack(torch_cuda, opt125m, engine, shape, monkeypatch):
     """Every launch shape of the scatter and gather kernels gives the same bytes."""
     for k, v in shape.items():
@@ -411,7 +412,8 @@ def test_single_hip_runtime(torch_cuda):
 
 
 @pytest.mark.parametrize("shape", [{"SLLM_K1_UNROLL": "2"}, {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1"},
-                                   {"SLLM_K1_BLOCKS": "1024"}, {"SLLM_K1_BLOCKS": "7", "SLLM_K1_UNROLL": "4"}])
+                                   {"SLLM_K1_BLOCKS": "1024"}, {"SLLM_K1_BLOCKS": "7", "SLLM_K1_UNROLL": "4"},
+                                   {"SLLM_K1_STREAM_BLOCKS": "1"}, {"SLLM_K1_STREAM_BLOCKS": "1024"}])
 def test_gather_shapes(torch_cuda, opt125m, shape, monkeypatch):
     """Every launch shape of the chunk gather gives the same bytes."""
     for k, v in shape.items():
