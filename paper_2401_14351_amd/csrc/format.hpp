@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <string>
+#include <string_view>
 #include <unordered_map>
 #include <vector>
 
@@ -22,7 +23,8 @@ constexpr const char* kDataName = "sllm.part0";
 uint32_t itemsize(uint32_t dtype);  // 0 for an unknown dtype
 
 struct TensorRec {
-    std::string name;
+    uint64_t name_off = 0;  // the name's first byte in IndexData::names
+    uint32_t name_len = 0;  // bytes, without the NUL that follows it there
     uint32_t dtype = 0;
     uint32_t ndim = 0;
     int64_t shape[SLLM_MAX_NDIM] = {};
@@ -36,6 +38,19 @@ struct IndexData {
     uint64_t total = 0;       // T = sum align_up(s_i, A)
     uint64_t file_bytes = 0;  // F = align_up(T, 4096)
     std::vector<TensorRec> tensors;
+    // every tensor's name followed by a NUL, in record order: one buffer for
+    // all names instead of an allocation per name
+    std::string names;
+
+    const char* name(size_t i) const { return names.data() + tensors[i].name_off; }
+    std::string_view name_view(size_t i) const { return {names.data() + tensors[i].name_off, tensors[i].name_len}; }
+    // record t's name (len bytes at s)
+    void set_name(TensorRec& t, const char* s, size_t len) {
+        t.name_off = names.size();
+        t.name_len = (uint32_t)len;
+        names.append(s, len);
+        names.push_back('\0');
+    }
 };
 
 // CRC-32, IEEE 802.3 polynomial (reflected 0xEDB88320), as used by zlib/PNG.

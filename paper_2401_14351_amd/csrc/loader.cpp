@@ -709,7 +709,7 @@ namespace {
 void fill_info(const sllm_ckpt* h, uint32_t i, sllm_tensor_info* out) {
     const TensorRec& t = h->ix.tensors[i];
     std::memset(out, 0, sizeof *out);
-    out->name = t.name.c_str();
+    out->name = h->ix.name(i);
     out->dtype = t.dtype;
     out->ndim = t.ndim;
     for (uint32_t d = 0; d < t.ndim; ++d) out->shape[d] = t.shape[d];
@@ -734,7 +734,7 @@ extern "C" int32_t sllm_tensor_find(const sllm_ckpt* h, const char* name, sllm_t
     if (!h || !name || !out) return fail(SLLM_E_INVAL, "handle, name and out must be non-NULL");
     std::call_once(h->by_name_once, [h] {
         h->by_name.reserve(h->ix.tensors.size() * 2);
-        for (uint32_t i = 0; i < h->ix.tensors.size(); ++i) h->by_name.emplace(h->ix.tensors[i].name, i);
+        for (uint32_t i = 0; i < h->ix.tensors.size(); ++i) h->by_name.emplace(h->ix.name_view(i), i);
     });
     auto it = h->by_name.find(std::string_view(name));
     if (it == h->by_name.end()) return fail(SLLM_E_NOTFOUND, "no tensor named '%s'", name);

@@ -25,8 +25,8 @@ struct sllm_writer {
     uint64_t alignment = 256, chunk_size = 16ull << 20;
     uint32_t flags = 0;
     uint64_t cursor = 0;   // bytes of the partition written so far (buffered included)
-    std::vector<TensorRec> recs;
-    std::unordered_set<std::string> names;
+    IndexData ix;                          // records and names so far
+    std::unordered_set<std::string> names;  // for the duplicate check
     uint8_t* buf = nullptr;   // staging buffer for small writes
     size_t fill = 0;
     int32_t error = SLLM_OK;  // sticky: first failure
@@ -168,13 +168,13 @@ extern "C" int32_t sllm_writer_add(sllm_writer* w, const sllm_src_tensor* t) try
         return st;
     }
     TensorRec r;
-    r.name = t->name;
+    w->ix.set_name(r, t->name, std::strlen(t->name));
     r.dtype = t->dtype;
     r.ndim = t->ndim;
     for (uint32_t d = 0; d < t->ndim; ++d) r.shape[d] = t->shape[d];
     r.offset = off;
     r.nbytes = t->nbytes;
-    w->recs.push_back(std::move(r));
+    w->ix.tensors.push_back(r);
     return SLLM_OK;
 } SLLM_CATCH_ALL
 
@@ -187,7 +187,7 @@ extern "C" int32_t sllm_writer_close(sllm_writer* w) try {
         destroy(w, true);
         return fail(st, "writer failed earlier; partial files removed");
     }
-    IndexData ix;
+    IndexData& ix = w->ix;
     ix.alignment = w->alignment;
     ix.chunk_size = w->chunk_size;
     // T: the end of the last padded slot; F: T rounded up to whole 4 KiB blocks
@@ -201,10 +201,7 @@ extern "C" int32_t sllm_writer_close(sllm_writer* w) try {
         st = fail(SLLM_E_IO, "fsync %s: %s", w->data_path.c_str(), std::strerror(errno));
     if (st == SLLM_OK && ::close(w->fd) != 0) st = fail(SLLM_E_IO, "close %s: %s", w->data_path.c_str(), std::strerror(errno));
     w->fd = -1;
-    if (st == SLLM_OK) {
-        ix.tensors = std::move(w->recs);
-        st = write_file(w->index_path, encode_index(ix), (w->flags & SLLM_CONVERT_FSYNC) != 0);
-    }
+    if (st == SLLM_OK) st = write_file(w->index_path, encode_index(ix), (w->flags & SLLM_CONVERT_FSYNC) != 0);
     destroy(w, st != SLLM_OK);
     return st;
 } SLLM_CATCH_ALL

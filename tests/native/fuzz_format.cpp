@@ -4,6 +4,10 @@
 //  1. Random checkpoints go through the streaming writer; their index must
 //     decode, describe the aligned packed layout, and the data file must hold
 //     every tensor's bytes with zero padding.
+//  0. crc32 (table and carry-less-multiply paths) equals the bit-at-a-time
+//     definition of the reflected IEEE CRC-32 on every length up to 300,
+//     random longer buffers, unaligned starts, any initial value, and
+//     chained calls.
 //  2. A valid index is mutated (byte flips, truncation, growth), with its CRC
 //     recomputed half of the time so that field validation is reached.  The
 //     decoder must never fault, and any index it accepts must re-encode to
@@ -23,6 +27,18 @@
 #include "sllm.h"
 
 using namespace sllm;
+
+// The CRC-32 of zlib by its definition: a 32-bit shift register over the
+// message bits, least significant bit of each byte first, reflected
+// polynomial 0xEDB88320, register and result inverted.
+static uint32_t crc_bitwise(const uint8_t* p, size_t n, uint32_t crc) {
+    uint32_t c = ~crc;
+    for (size_t i = 0; i < n; ++i) {
+        c ^= p[i];
+        for (int b = 0; b < 8; ++b) c = (c & 1) ? (c >> 1) ^ 0xEDB88320u : c >> 1;
+    }
+    return ~c;
+}
 
 static std::string slurp(const std::string& path) {
     std::ifstream f(path, std::ios::binary);
@@ -45,6 +61,22 @@ int main(int argc, char** argv) {
     const long iters = std::atol(argv[2]);
     std::mt19937_64 rng(20240125);
     std::string valid;
+
+    {  // 0. CRC-32 against its definition
+        const char* check = "123456789";
+        CHECK(crc32(check, 9) == 0xCBF43926u);
+        std::vector<uint8_t> buf(4096 + 16);
+        for (auto& b : buf) b = (uint8_t)rng();
+        for (size_t n = 0; n <= 4096; n = n < 300 ? n + 1 : n + 1 + rng() % 97) {
+            const size_t off = rng() % 16;
+            const uint32_t init = (n % 3 == 0) ? 0u : (uint32_t)rng();
+            const uint8_t* p = buf.data() + off;
+            const uint32_t want = crc_bitwise(p, n, init);
+            CHECK(crc32(p, n, init) == want);
+            const size_t cut = n ? rng() % (n + 1) : 0;  // chained: crc of a then b == crc of a + b
+            CHECK(crc32(p + cut, n - cut, crc32(p, cut, init)) == want);
+        }
+    }
 
     for (int round = 0; round < 60; ++round) {
         sllm_convert_opts o{1ull << (rng() % 13), 1 + rng() % 5000, 0, 0};
