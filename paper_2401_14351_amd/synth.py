@@ -162,6 +162,18 @@ def lora(size: str = "70b", rank: int = 32, seed: int = 1006) -> CheckpointSpec:
     return CheckpointSpec(f"lora-{size}-r{rank}", seed, alignment=256, chunk_size=16 * MiB, tensors=t)
 
 
+def huge_tensor(seed: int = 1007) -> CheckpointSpec:
+    """One int8 tensor of 65,537 x 65,539 = 4,295,229,443 bytes (just over
+    2^32) between small tensors of odd byte sizes, uniform random bytes,
+    packed densely (A = 1): the tensor starts at an odd file offset, and
+    bytes inside it lie more than 4 GiB from its start."""
+    t = [TensorSpec("head.bias", "bf16", (1531,), "bytes"),
+         TensorSpec("huge.weight", "i8", (65537, 65539), "bytes"),
+         TensorSpec("tail.scale", "f32", (3,), "bytes"),
+         TensorSpec("tail.weight", "f16", (4097, 3), "bytes")]
+    return CheckpointSpec("huge-tensor", seed, alignment=1, chunk_size=16 * MiB, tensors=t)
+
+
 def _prime_factors(n: int) -> List[int]:
     out, p = [], 2
     while p * p <= n:
@@ -313,7 +325,8 @@ def materialize(spec: CheckpointSpec, threads: Optional[int] = None) -> List[np.
 def config(name: str) -> CheckpointSpec:
     """The five benchmark workloads by name, plus the capped stress variant
     (and that variant converted densely, for repacks whose shifts are not
-    multiples of 16 bytes)."""
+    multiples of 16 bytes), the LoRA adapter and the checkpoint with one
+    tensor over 4 GiB."""
     if name == "opt-125m":
         return opt_125m()
     if name.startswith("llama-2-"):
@@ -328,6 +341,8 @@ def config(name: str) -> CheckpointSpec:
         return spec
     if name == "lora-70b-r32":
         return lora("70b", 32)
+    if name == "huge-tensor":
+        return huge_tensor()
     raise KeyError(name)
 
 

@@ -165,6 +165,53 @@ def test_stress_8g_every_path(torch_cuda):
     release(torch)
 
 
+def test_tensor_over_4gib(torch_cuda):
+    """One tensor of 4,295,229,443 bytes packed densely between odd-sized
+    ones: in-tensor offsets past 2^32 in every path.  At A2 = 256 its source
+    shift is -10 bytes, so K1-scatter and K2 move it through the byte
+    funnel.  Cached by both engines in the file layout and into A2 = 256,
+    K2's repack of the file-layout image, and a streamed K1-scatter load."""
+    torch = torch_cuda
+    spec = synth.config("huge-tensor")
+    assert max(t.nbytes for t in spec.tensors) > 1 << 32
+    d, digests = converted(spec)
+    sizes = [t.nbytes for t in spec.tensors]
+    offsets, T = oracle.plan_layout(sizes, spec.alignment)
+    d2, T2 = oracle.plan_layout(sizes, 256)
+    assert (offsets[1] - d2[1]) % 16 != 0
+    say("huge-tensor: T", T, "T2", T2)
+    s = torch.cuda.current_stream()
+    buf = fresh(torch, T)
+    out = fresh(torch, T2)
+    with binding.Pool(spec.chunk_size, -(-T // spec.chunk_size)) as pool:
+        pool.cache(d, io_threads=8)
+        for engine in ("kernel", "sdma"):
+            buf.fill_(SENTINEL)
+            with binding.Checkpoint(d, pool=pool, engine=engine) as ck:
+                ck.load_into(buf, s)
+                s.synchronize()
+            check(torch, buf, spec, offsets, T, digests, f"huge-tensor file layout by {engine}")
+            out.fill_(SENTINEL)
+            with binding.Checkpoint(d, pool=pool, engine=engine, dev_alignment=256) as ck:
+                assert [t.offset for t in ck.tensors()] == d2
+                ck.load_into(out, s)
+                s.synchronize()
+            check(torch, out, spec, d2, T2, digests, f"huge-tensor A2=256 by {engine}")
+        out.fill_(SENTINEL)
+        with binding.Checkpoint(d, pool=pool, dev_alignment=256) as ck:
+            ck.repack(buf, out, s)
+            s.synchronize()
+        check(torch, out, spec, d2, T2, digests, "huge-tensor K2 repack to A2=256")
+        pool.evict(d)
+    out.fill_(SENTINEL)
+    with binding.Checkpoint(d, dev_alignment=256, io_threads=8, ring_slots=16) as ck:
+        ck.load_into(out, s)
+        s.synchronize()
+    check(torch, out, spec, d2, T2, digests, "huge-tensor streamed K1-scatter to A2=256")
+    del buf, out
+    release(torch)
+
+
 @pytest.mark.parametrize("C_mib", [4, 16, 64])
 def test_llama2_13b_chunk_sizes(torch_cuda, C_mib):
     """26.0 GB, 363 tensors (a 2 KiB file tail), the chunk-size sweep: the
