@@ -37,7 +37,8 @@ HBM_PEAK_GBPS = 8000.0      # MI355X HBM3E
 DATA = {"llama": "synthetic (seeded N(0,0.02) bf16 weights, RMSNorm weights 1.0)",
         "opt-125m": "synthetic (seeded N(0,0.02) fp16 weights)",
         "stress": "synthetic (seeded uniform random bytes, f32/f16/bf16/i8 tensors)",
-        "lora": "synthetic (seeded N(0,0.02) bf16 LoRA A/B matrices)"}
+        "lora": "synthetic (seeded N(0,0.02) bf16 LoRA A/B matrices)",
+        "huge-tensor": "synthetic (seeded uniform random bytes; one int8 tensor over 4 GiB)"}
 REGIME = {"dram": "warm host DRAM (pinned pool)",
           "ring": "file through pinned ring slots (buffered reads)",
           "direct": "file through pinned ring slots (O_DIRECT reads)"}
@@ -801,7 +802,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama-2-7b",
-                    choices=list(synth.WORKLOADS) + ["stress-8g", "stress-8g-dense", "lora-70b-r32"])
+                    choices=list(synth.WORKLOADS) + ["stress-8g", "stress-8g-dense", "lora-70b-r32", "huge-tensor"])
     ap.add_argument("--engine", default="kernel", choices=["kernel", "sdma"])
     ap.add_argument("--regime", default="dram", choices=["dram", "ring", "direct"],
                     help="dram: partition cached in the pinned pool (graded); ring: streamed from the file "
