@@ -253,6 +253,20 @@ def test_open_rejects_truncated_index(L, ckpt):
     assert _open_code(L, ckpt)[0] == -3
 
 
+def test_close_is_safe_to_repeat(L, ckpt):
+    """Closing nothing is a no-op for every handle type, and the binding's
+    close() may run twice (the second call does nothing)."""
+    assert L.sllm_close(None) == 0
+    assert L.sllm_pool_destroy(None) == 0
+    L.sllm_estimator_destroy(None)  # returns nothing; must not crash
+    ck = binding.Checkpoint(str(ckpt), index_only=True)
+    assert ck.total_bytes > 0
+    ck.close()
+    ck.close()
+    with binding.Checkpoint(str(ckpt), index_only=True) as ck2:
+        ck2.close()  # closed inside the block; leaving it closes nothing more
+
+
 def test_open_missing_dir(L, tmp_path):
     assert _open_code(L, tmp_path / "nope")[0] == -2
 
