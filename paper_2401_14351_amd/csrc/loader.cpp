@@ -254,6 +254,16 @@ uint64_t batch_target_bytes() {
     return (end && *end == '\0' && v >= 0) ? (uint64_t)v << 20 : kDefault;
 }
 
+// Leading chunks of a streamed load read in pieces (SLLM_SPLIT_CHUNKS;
+// default: as many as there are I/O threads).
+uint64_t split_chunks(uint32_t io_threads) {
+    const char* s = std::getenv("SLLM_SPLIT_CHUNKS");
+    if (!s || !*s) return io_threads;
+    char* end = nullptr;
+    const long v = std::strtol(s, &end, 10);
+    return (end && *end == '\0' && v >= 0) ? (uint64_t)v : io_threads;
+}
+
 // After a successful streamed load with kept slots, hand them to the pool as
 // its cached copy of the checkpoint; the handle then loads from the cache.
 // If another handle cached the same file meanwhile, the slots stay with this
@@ -402,8 +412,14 @@ int32_t load_streamed(sllm_ckpt* h, uint8_t* dst, hipStream_t user) {
     plan.max_batch = max_batch;
     plan.target = std::max<uint64_t>(1, batch_target_bytes() / C);
     plan.keep = h->keep;
-    auto read = [h](uint64_t k, uint32_t si, uint64_t len, uint64_t* bounced) {
-        return read_chunk(h->file, h->slots[si].host, len, k * h->chunk, h->data_path, bounced);
+    // the first chunks are read in pieces of at least 1 MiB by all readers
+    // together (SLLM_SPLIT_CHUNKS of them, default one per reader; 0 reads
+    // every chunk whole), aligned for direct reads
+    plan.split_chunks = split_chunks(h->io_threads);
+    plan.split_min = 1ull << 20;
+    plan.split_align = h->file.direct ? std::max<uint64_t>(h->file.dio_align, 4096) : 4096;
+    auto read = [h](uint64_t k, uint32_t si, uint64_t off, uint64_t len, uint64_t* bounced) {
+        return read_chunk(h->file, h->slots[si].host + off, len, k * h->chunk + off, h->data_path, bounced);
     };
     std::vector<TraceEvent> trace;
     const char* tpath = trace_path();

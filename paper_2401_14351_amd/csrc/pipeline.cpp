@@ -68,57 +68,112 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         cv_ready.notify_all();
     };
 
-    // a reader takes a free slot (with keep: slot k) and then the next chunk
-    // number, reads the chunk into the slot and queues it.  Slots go to
-    // chunks in chunk order, so a chunk the sink waits for is always held
-    // by a reader or already queued: a sink that consumes chunks in order
-    // cannot be left waiting for a chunk with every slot held by later ones.
+    // The first split_chunks chunks are read in pieces: the reader that
+    // takes such a chunk publishes its other pieces, and readers take open
+    // pieces before they start a chunk of their own.  Only the newest split
+    // chunk can have pieces nobody took yet.
+    struct Split {
+        uint64_t k = 0, len = 0, piece = 0;
+        uint32_t si = 0, pieces = 0, taken = 0, left = 0;
+    };
+    std::vector<Split> splits;  // split chunks not yet read completely (guarded by mu)
+    auto open_split = [&]() -> Split* {
+        return !splits.empty() && splits.back().taken < splits.back().pieces ? &splits.back() : nullptr;
+    };
+    const uint32_t nt = (uint32_t)std::min<uint64_t>(p.io_threads ? p.io_threads : 1, n);
+    auto pieces_of = [&](uint64_t k, uint64_t len, uint64_t* piece) -> uint32_t {
+        if (k >= p.split_chunks || nt < 2 || p.split_min == 0) return 1;
+        const uint64_t want = std::min<uint64_t>(nt, len / p.split_min);
+        if (want < 2) return 1;
+        const uint64_t a = std::max<uint64_t>(1, p.split_align);
+        *piece = ceil_div(ceil_div(len, want), a) * a;
+        return (uint32_t)ceil_div(len, *piece);
+    };
+
+    // a reader takes an open piece, else a free slot (with keep: slot k) and
+    // then the next chunk number, reads it into the slot and queues the
+    // chunk once all of it is read.  Slots go to chunks in chunk order, so a
+    // chunk the sink waits for is always being read or already queued: a
+    // sink that consumes chunks in order cannot be left waiting for a chunk
+    // with every slot held by later ones.
     auto reader = [&](uint32_t thread) {
         for (;;) {
-            uint64_t k;
-            uint32_t si;
+            uint64_t k = 0, off = 0, len = 0;
+            uint32_t si = 0;
+            bool piece = false;
             {
                 const double w0 = now_s();
                 std::unique_lock<std::mutex> lk(mu);
-                if (p.keep) {
-                    if (stop) return;
-                    k = next.fetch_add(1);
-                    if (k >= n) return;
-                    si = (uint32_t)k;
-                } else {
-                    cv_free.wait(lk, [&] { return stop || next.load() >= n || !free_q.empty(); });
+                if (!p.keep) {
+                    cv_free.wait(lk, [&] { return stop || open_split() || next.load() >= n || !free_q.empty(); });
                     starved_ns += (uint64_t)((now_s() - w0) * 1e9);
-                    if (stop || next.load() >= n) return;
+                }
+                if (stop) return;
+                if (Split* sp = open_split()) {
+                    k = sp->k;
+                    si = sp->si;
+                    off = (uint64_t)sp->taken * sp->piece;
+                    len = std::min(sp->piece, sp->len - off);
+                    ++sp->taken;
+                    piece = true;
+                } else {
+                    if (next.load() >= n) return;
                     k = next.fetch_add(1);
-                    si = free_q.front();
-                    free_q.pop_front();
+                    if (p.keep) {
+                        si = (uint32_t)k;
+                    } else {
+                        si = free_q.front();
+                        free_q.pop_front();
+                    }
+                    const uint64_t chunk_len = std::min(C, p.read_end - k * C);
+                    uint64_t piece_len = 0;
+                    const uint32_t np = pieces_of(k, chunk_len, &piece_len);
+                    len = chunk_len;
+                    if (np > 1) {
+                        Split sp;
+                        sp.k = k;
+                        sp.len = chunk_len;
+                        sp.piece = piece_len;
+                        sp.si = si;
+                        sp.pieces = np;
+                        sp.taken = 1;
+                        sp.left = np;
+                        splits.push_back(sp);
+                        len = piece_len;
+                        piece = true;
+                        cv_free.notify_all();  // idle readers take the other pieces
+                    }
+                    trace(TraceEvent::kReadBegin, k, si, thread);
                 }
                 ++reading;
             }
-            const uint64_t off = k * C, len = std::min(C, p.read_end - off);
             uint64_t bounced = 0;
-            trace(TraceEvent::kReadBegin, k, si, thread);
             const double r0 = now_s();
             range_push("sllm read chunk");
-            const int32_t st = read(k, si, len, &bounced);
+            const int32_t st = read(k, si, off, len, &bounced);
             range_pop();
             busy_ns += (uint64_t)((now_s() - r0) * 1e9);
-            if (st == SLLM_OK) trace(TraceEvent::kReadEnd, k, si, thread);
             std::lock_guard<std::mutex> g(mu);
             --reading;
             if (st != SLLM_OK) {
-                if (!p.keep) free_q.push_back(si);
+                if (!p.keep && !piece) free_q.push_back(si);
                 set_error(st);
                 return;
             }
             bytes_read += len;
             bytes_bounced += bounced;
+            if (piece) {
+                auto it = std::find_if(splits.begin(), splits.end(), [&](const Split& x) { return x.k == k; });
+                if (--it->left > 0) continue;
+                splits.erase(it);
+            }
+            trace(TraceEvent::kReadEnd, k, si, thread);
             ready_q.push_back({k, si});
             cv_ready.notify_one();
         }
     };
 
-    const uint32_t nt = (uint32_t)std::min<uint64_t>(p.io_threads ? p.io_threads : 1, n);
+
     std::vector<std::thread> threads;
     try {
         threads.reserve(nt);
@@ -176,9 +231,10 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         {
             const double w0 = now_s();
             std::unique_lock<std::mutex> lk(mu);
-            // readers are reading, or will start on a free slot (a chunk of
-            // their own when slots are kept)
-            const bool readers_busy = reading > 0 || (next.load() < n && (p.keep || !free_q.empty()));
+            // readers are reading, will take an open piece, or will start on
+            // a free slot (a chunk of their own when slots are kept)
+            const bool readers_busy =
+                reading > 0 || open_split() || (next.load() < n && (p.keep || !free_q.empty()));
             if (ready_q.empty() && !stop) {
                 if (!readers_busy && !inflight.empty())
                     wait_sink = true;  // every slot is with the sink

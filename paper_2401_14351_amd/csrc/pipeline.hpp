@@ -68,6 +68,14 @@ struct StreamPlan {
     uint32_t max_batch = 1;   // chunks per move()
     uint64_t target = 1;      // chunks a batch waits to collect while the sink is still busy
     bool keep = false;        // chunk k always uses slot k and slots are never refilled
+    // The first split_chunks chunks are read in pieces by all readers
+    // together, one chunk after another, so that the next tier gets its first
+    // chunk after a fraction of one chunk's read time; later chunks are read
+    // whole.  Pieces hold at least split_min bytes and start at multiples of
+    // split_align bytes of the chunk (a direct read's alignment).
+    uint64_t split_chunks = 0;
+    uint64_t split_min = 1;
+    uint64_t split_align = 1;
     std::vector<TraceEvent>* trace = nullptr;  // when set, every chunk's steps are appended
 };
 
@@ -81,9 +89,11 @@ struct StreamStats {
     double reader_starved_s = 0;
 };
 
-// Reads chunk k (`len` bytes from file offset kC) into slot `slot`; may add
-// to *bounced the bytes it staged through a bounce buffer.
-using ChunkReader = std::function<int32_t(uint64_t k, uint32_t slot, uint64_t len, uint64_t* bounced)>;
+// Reads bytes [off, off + len) of chunk k (file offset kC + off) into bytes
+// [off, off + len) of slot `slot`; may add to *bounced the bytes it staged
+// through a bounce buffer.  A whole chunk is read with off = 0.
+using ChunkReader =
+    std::function<int32_t(uint64_t k, uint32_t slot, uint64_t off, uint64_t len, uint64_t* bounced)>;
 
 // Wait for every batch still in flight (from an earlier load) and forget it;
 // with a trace, append each chunk's kDone at `t` seconds after `t_start`

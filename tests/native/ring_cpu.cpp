@@ -180,7 +180,14 @@ struct Case {
     uint32_t slots, threads, max_batch;
     uint64_t target;
     bool keep;
+    uint64_t split_chunks = 0, split_min = 1, split_align = 1;  // leading chunks read in pieces
 };
+
+// A piece must lie inside its chunk and start at a multiple of the alignment.
+void check_piece(const Case& cs, uint64_t k, uint64_t off, uint64_t len) {
+    const uint64_t chunk_len = std::min(cs.C, cs.T - k * cs.C);
+    if (off + len > chunk_len || (off % cs.split_align) != 0 || (off && k >= cs.split_chunks)) ++g_violations;
+}
 
 // One sink, several loads: clean ones, then (optionally) one with an
 // injected error, then a clean one again.
@@ -196,7 +203,7 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
     std::deque<InFlightBatch> inflight;
     std::atomic<int64_t> fail_read_at{-1};
     std::mutex rng_mu;
-    ChunkReader read = [&](uint64_t k, uint32_t si, uint64_t len, uint64_t* bounced) -> int32_t {
+    ChunkReader read = [&](uint64_t k, uint32_t si, uint64_t off, uint64_t len, uint64_t* bounced) -> int32_t {
         uint32_t delay;
         {
             std::lock_guard<std::mutex> g(rng_mu);
@@ -205,8 +212,9 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
         if (delay) std::this_thread::sleep_for(std::chrono::microseconds(delay));
         if ((int64_t)k == fail_read_at.load()) return fail(SLLM_E_IO, "injected read error at chunk %llu", (unsigned long long)k);
         if (cs.keep && si != k) ++g_violations;
+        check_piece(cs, k, off, len);
         sink.check_free(si);
-        std::memcpy(slots.data() + (uint64_t)si * cs.C, file.data() + k * cs.C, len);
+        std::memcpy(slots.data() + (uint64_t)si * cs.C + off, file.data() + k * cs.C + off, len);
         *bounced += len & 1;
         return SLLM_OK;
     };
@@ -219,6 +227,9 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
     plan.max_batch = cs.max_batch;
     plan.target = cs.target;
     plan.keep = cs.keep;
+    plan.split_chunks = cs.split_chunks;
+    plan.split_min = cs.split_min;
+    plan.split_align = cs.split_align;
     for (int load = 0; load < 4; ++load) {
         const bool faulty = inject && load == 2 && n > 0;
         if (faulty) {
@@ -387,15 +398,16 @@ int run_in_order_case(const Case& cs, uint64_t seed) {
     for (int load = 0; load < 3; ++load) {
         std::fill(dst.begin(), dst.end(), 0xEE);
         InOrderSink sink(slots, cs.C, cs.slots, dst, cs.C, cs.T);
-        ChunkReader read = [&](uint64_t k, uint32_t si, uint64_t len, uint64_t*) -> int32_t {
+        ChunkReader read = [&](uint64_t k, uint32_t si, uint64_t off, uint64_t len, uint64_t*) -> int32_t {
             uint32_t delay;
             {
                 std::lock_guard<std::mutex> g(rng_mu);
                 delay = (uint32_t)(rng() % 200);
             }
             if (delay) std::this_thread::sleep_for(std::chrono::microseconds(delay));
+            check_piece(cs, k, off, len);
             sink.check_free(si);
-            std::memcpy(slots.data() + (uint64_t)si * cs.C, file.data() + k * cs.C, len);
+            std::memcpy(slots.data() + (uint64_t)si * cs.C + off, file.data() + k * cs.C + off, len);
             return SLLM_OK;
         };
         StreamPlan plan;
@@ -406,6 +418,9 @@ int run_in_order_case(const Case& cs, uint64_t seed) {
         plan.n_slots = cs.slots;
         plan.max_batch = 1;
         plan.target = 1;
+        plan.split_chunks = cs.split_chunks;
+        plan.split_min = cs.split_min;
+        plan.split_align = cs.split_align;
         std::deque<InFlightBatch> inflight;
         StreamStats ss;
         int32_t st = run_stream(plan, read, sink, inflight, &ss);
@@ -425,6 +440,15 @@ int run_in_order_case(const Case& cs, uint64_t seed) {
 
 }  // namespace
 
+// Two cases in three read some leading chunks (sometimes all) in pieces.
+void random_split(Case& cs, std::mt19937_64& rng) {
+    if (rng() % 3 == 0) return;
+    cs.split_chunks = rng() % 4 == 0 ? 1000000 : rng() % 6;
+    cs.split_min = 1 + rng() % 4;
+    const uint64_t aligns[] = {1, 2, 4, 8};
+    cs.split_align = aligns[rng() % 4];
+}
+
 int main(int argc, char** argv) {
     const int n_cases = argc > 1 ? std::atoi(argv[1]) : 300;
     std::mt19937_64 rng(20240114351ull);
@@ -439,11 +463,14 @@ int main(int argc, char** argv) {
         cs.max_batch = rng() % 3 == 0 ? 1 : 1 + (uint32_t)(rng() % 8);
         cs.target = 1 + rng() % 4;
         cs.keep = rng() % 5 == 0;
+        random_split(cs, rng);
         const int inject = (int)(i % 3);  // none, read error, move error
         if (run_case(cs, rng(), inject) != 0) {
-            std::printf("case %d failed: T=%llu C=%llu slots=%u threads=%u max_batch=%u target=%llu keep=%d inject=%d\n",
+            std::printf("case %d failed: T=%llu C=%llu slots=%u threads=%u max_batch=%u target=%llu keep=%d inject=%d "
+                        "split=%llu/%llu/%llu\n",
                         i, (unsigned long long)cs.T, (unsigned long long)cs.C, cs.slots, cs.threads, cs.max_batch,
-                        (unsigned long long)cs.target, (int)cs.keep, inject);
+                        (unsigned long long)cs.target, (int)cs.keep, inject, (unsigned long long)cs.split_chunks,
+                        (unsigned long long)cs.split_min, (unsigned long long)cs.split_align);
             ++failures;
             if (failures > 5) break;
         }
@@ -455,9 +482,12 @@ int main(int argc, char** argv) {
         cs.T = 1 + rng() % (40 * cs.C);
         cs.slots = 1 + (uint32_t)(rng() % 4);
         cs.threads = 1 + (uint32_t)(rng() % 6);
+        random_split(cs, rng);
         if (run_in_order_case(cs, rng()) != 0) {
-            std::printf("in-order case %d failed: T=%llu C=%llu slots=%u threads=%u\n", i, (unsigned long long)cs.T,
-                        (unsigned long long)cs.C, cs.slots, cs.threads);
+            std::printf("in-order case %d failed: T=%llu C=%llu slots=%u threads=%u split=%llu/%llu/%llu\n", i,
+                        (unsigned long long)cs.T, (unsigned long long)cs.C, cs.slots, cs.threads,
+                        (unsigned long long)cs.split_chunks, (unsigned long long)cs.split_min,
+                        (unsigned long long)cs.split_align);
             ++failures;
         }
     }
