@@ -72,6 +72,28 @@ struct sllm_ckpt {
 
 namespace {
 
+// Copy streams outlive the handles that use them.  Creating a handle's
+// streams and destroying them again at close costs most of a millisecond,
+// as long as a small checkpoint's whole transfer, so a closed handle leaves
+// its streams, idle, with their fork/join events here for the next handle
+// on the same device.  They live until the process ends.
+struct StreamSet {
+    int device = 0;
+    std::vector<hipStream_t> streams;
+    std::vector<hipEvent_t> join_ev;
+    hipEvent_t fork_ev = nullptr;
+};
+constexpr size_t kMaxIdleStreamSets = 32;
+std::mutex g_idle_mu;
+std::vector<StreamSet> g_idle_sets;
+
+// Take an idle set of n streams of `device`; false if there is none.
+bool take_stream_set(int device, uint32_t n, sllm_ckpt* h);
+
+// Park the handle's copy streams (synchronized by the caller); false if the
+// list is full or the set is incomplete, and then the caller destroys them.
+bool park_stream_set(sllm_ckpt* h);
+
 void release(sllm_ckpt* h) {
     const bool used_hip = !h->streams.empty() || !h->slots.empty() || h->fork_ev || h->t0_ev || h->t1_ev ||
                           h->layout.d_off || h->layout.staging;
@@ -82,12 +104,15 @@ void release(sllm_ckpt* h) {
         for (const InFlightBatch& b : h->inflight) (void)hipEventSynchronize(h->slots[b.token].done);
         for (Slot& s : h->slots)
             if (s.done) (void)hipEventDestroy(s.done);
-        for (hipEvent_t e : h->join_ev)
+        if (!park_stream_set(h)) {
+            for (hipEvent_t e : h->join_ev)
+                if (e) (void)hipEventDestroy(e);
+            if (h->fork_ev) (void)hipEventDestroy(h->fork_ev);
+            for (hipStream_t s : h->streams)
+                if (s) (void)hipStreamDestroy(s);
+        }
+        for (hipEvent_t e : {h->t0_ev, h->t1_ev})
             if (e) (void)hipEventDestroy(e);
-        for (hipEvent_t e : {h->fork_ev, h->t0_ev, h->t1_ev})
-            if (e) (void)hipEventDestroy(e);
-        for (hipStream_t s : h->streams)
-            if (s) (void)hipStreamDestroy(s);
         device_layout_free(&h->layout);
     }
     if (h->keep_table) pool_free_table(h->pool, h->keep_table);
@@ -102,11 +127,44 @@ void release(sllm_ckpt* h) {
     delete h;
 }
 
-// The copy streams and their fork/join events, created at the first load
-// that needs them (a cached load by the kernel engine runs on the caller's
-// stream alone, so opening such a handle creates no HIP objects).
+bool take_stream_set(int device, uint32_t n, sllm_ckpt* h) {
+    std::lock_guard<std::mutex> g(g_idle_mu);
+    for (auto it = g_idle_sets.begin(); it != g_idle_sets.end(); ++it) {
+        if (it->device != device || it->streams.size() != n) continue;
+        h->streams = std::move(it->streams);
+        h->join_ev = std::move(it->join_ev);
+        h->fork_ev = it->fork_ev;
+        g_idle_sets.erase(it);
+        return true;
+    }
+    return false;
+}
+
+bool park_stream_set(sllm_ckpt* h) {
+    if (h->streams.empty() || !h->fork_ev || h->join_ev.size() != h->streams.size()) return false;
+    for (size_t i = 0; i < h->streams.size(); ++i)
+        if (!h->streams[i] || !h->join_ev[i]) return false;
+    std::lock_guard<std::mutex> g(g_idle_mu);
+    if (g_idle_sets.size() >= kMaxIdleStreamSets) return false;
+    StreamSet set;
+    set.device = h->device;
+    set.streams = std::move(h->streams);
+    set.join_ev = std::move(h->join_ev);
+    set.fork_ev = h->fork_ev;
+    g_idle_sets.push_back(std::move(set));
+    h->streams.clear();
+    h->join_ev.clear();
+    h->fork_ev = nullptr;
+    return true;
+}
+
+// The copy streams and their fork/join events, taken at the first load that
+// needs them (a cached load by the kernel engine runs on the caller's stream
+// alone, so opening such a handle creates no HIP objects): an idle set a
+// closed handle left, else new ones.
 int32_t ensure_streams(sllm_ckpt* h) {
     if (!h->streams.empty()) return SLLM_OK;
+    if (take_stream_set(h->device, h->n_streams, h)) return SLLM_OK;
     h->streams.assign(h->n_streams, nullptr);
     h->join_ev.assign(h->n_streams, nullptr);
     for (uint32_t i = 0; i < h->n_streams; ++i) {
