@@ -41,6 +41,10 @@
  *                         done times to this CSV file.
  *   SLLM_ROCTX=1          host stages become roctx ranges (rocprofv3
  *                         --marker-trace); the roctx library is loaded then.
+ *   SLLM_READ_STREAM=0    buffered chunks are read straight into pinned
+ *                         memory (default: through a 1 MiB per-thread buffer
+ *                         copied on with streaming stores, so that the GPU
+ *                         reads them from DRAM, not from dirty CPU caches).
  *   SLLM_READ_MAPPED=1    buffered files are mapped and chunks copied with
  *                         streaming stores instead of read with pread.
  *   SLLM_BATCH_TARGET_MB  bytes a streamed gather batch collects (64).

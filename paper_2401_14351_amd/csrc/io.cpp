@@ -175,6 +175,38 @@ int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const
     return e ? read_error(e, path, off) : SLLM_OK;
 }
 
+namespace {
+
+// 1 MiB: small enough to stay in the reader core's caches between the read
+// into it and the copy out of it
+constexpr uint64_t kStreamBytes = 1u << 20;
+
+uint8_t* stream_buffer() {
+    thread_local Bounce b;
+    if (!b.p && posix_memalign(&b.p, 4096, kStreamBytes) != 0) b.p = nullptr;
+    return static_cast<uint8_t*>(b.p);
+}
+
+// Buffered read through a small cache-resident buffer, copied into dst with
+// streaming stores: a pinned chunk then holds its bytes in DRAM rather than
+// dirty in the CPU's caches, where the GPU's reads of it would have to be
+// served by snoops (measured slower at the start of a streamed load).
+int32_t pread_streamed(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path) {
+    uint8_t* b = stream_buffer();
+    if (!b) return pread_full(f, dst, n, off, path);
+    uint8_t* d = static_cast<uint8_t*>(dst);
+    for (uint64_t done = 0; done < n;) {
+        const uint64_t k = n - done < kStreamBytes ? n - done : kStreamBytes;
+        const int e = pread_exact(f.fd, b, k, off + done);
+        if (e) return read_error(e, path, off + done);
+        copy_stream(d + done, b, k);
+        done += k;
+    }
+    return SLLM_OK;
+}
+
+}  // namespace
+
 int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
                    uint64_t* bounced) {
     if (!f.direct && f.map) {
@@ -203,7 +235,7 @@ int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const
         }
         return SLLM_OK;
     }
-    if (!f.direct) return pread_full(f, dst, n, off, path);
+    if (!f.direct) return stream_reads() ? pread_streamed(f, dst, n, off, path) : pread_full(f, dst, n, off, path);
     if (f.direct_into_pinned->load() != 0) {
         int e = pread_exact(f.fd, dst, n, off);
         if (e == 0) {
@@ -233,6 +265,11 @@ void drop_cache(const DataFile& f) { (void)::posix_fadvise(f.fd, 0, 0, POSIX_FAD
 bool mapped_reads() {
     const char* s = std::getenv("SLLM_READ_MAPPED");
     return s && *s == '1';
+}
+
+bool stream_reads() {
+    const char* s = std::getenv("SLLM_READ_STREAM");
+    return !(s && *s == '0');
 }
 
 }  // namespace sllm

@@ -37,10 +37,12 @@ int32_t pread_full(const DataFile& f, void* buf, uint64_t n, uint64_t off, const
 // straight into `dst`; where the kernel refuses direct transfers into that
 // memory (EFAULT: the pages cannot be pinned for I/O), they go through a
 // 16 MiB aligned per-thread bounce buffer instead, and *bounced counts them.
-// A buffered file with a mapping has the chunk's pages populated first
-// (which reports a range past the end of the file as an I/O error instead
-// of faulting) and then copied with non-temporal stores, so the destination
-// lines are written without first being read.
+// A buffered read goes through a 1 MiB per-thread buffer copied on with
+// streaming stores (see stream_reads).  A buffered file with a mapping has
+// the chunk's pages populated first (which reports a range past the end of
+// the file as an I/O error instead of faulting) and then copied with
+// non-temporal stores, so the destination lines are written without first
+// being read.
 int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const std::string& path,
                    uint64_t* bounced);
 
@@ -50,5 +52,10 @@ void drop_cache(const DataFile& f);
 // Whether buffered files are mapped and copied with streaming stores
 // (SLLM_READ_MAPPED=1) instead of read with pread.
 bool mapped_reads();
+
+// Whether buffered reads go through a small per-thread buffer and are
+// copied into the destination with streaming stores (the default;
+// SLLM_READ_STREAM=0 reads into the destination directly).
+bool stream_reads();
 
 }  // namespace sllm

@@ -1,8 +1,9 @@
 // CPU-only check of the chunk reader (csrc/io.cpp), built with AddressSanitizer
 // and UndefinedBehaviorSanitizer by tests/test_sanitize.py.
 //
-// For buffered files read with pread and read through the file mapping with
-// streaming stores (SLLM_READ_MAPPED=1): random chunk offsets and lengths,
+// For buffered files read with pread, read with pread through a small buffer
+// copied with streaming stores (SLLM_READ_STREAM=1), and read through the file
+// mapping with streaming stores (SLLM_READ_MAPPED=1): random chunk offsets and lengths,
 // destinations at every alignment mod 32, the bytes equal the file's; after
 // the file is truncated, a chunk past the new end is an I/O error (not a
 // fault) and a chunk before it still reads.
@@ -21,8 +22,11 @@
 
 using namespace sllm;
 
-static int check(const std::string& path, const std::vector<uint8_t>& bytes, bool mapped, std::mt19937_64& rng) {
+// mode 0: pread, 1: pread through the streaming buffer, 2: mapped
+static int check(const std::string& path, const std::vector<uint8_t>& bytes, int mode, std::mt19937_64& rng) {
+    const bool mapped = mode == 2;
     setenv("SLLM_READ_MAPPED", mapped ? "1" : "0", 1);
+    setenv("SLLM_READ_STREAM", mode == 1 ? "1" : "0", 1);
     DataFile f;
     if (open_data(path, false, &f) != SLLM_OK) {
         std::printf("open failed: %s\n", sllm_last_error());
@@ -45,8 +49,8 @@ static int check(const std::string& path, const std::vector<uint8_t>& bytes, boo
         }
         if (std::memcmp(buf.data() + shift, bytes.data() + off, n) != 0 || buf[shift + n] != 0xEE ||
             (shift && buf[shift - 1] != 0xEE)) {
-            std::printf("bytes differ at %llu (%llu bytes, shift %llu, mapped %d)\n", (unsigned long long)off,
-                        (unsigned long long)n, (unsigned long long)shift, (int)mapped);
+            std::printf("bytes differ at %llu (%llu bytes, shift %llu, mode %d)\n", (unsigned long long)off,
+                        (unsigned long long)n, (unsigned long long)shift, mode);
             return 1;
         }
     }
@@ -60,7 +64,7 @@ static int check(const std::string& path, const std::vector<uint8_t>& bytes, boo
     if (truncate(path.c_str(), (off_t)cut) != 0) return 1;
     const int32_t st = read_chunk(f, buf.data(), 1 << 20, cut + 8192, path, nullptr);
     if (st != SLLM_E_IO) {
-        std::printf("read past a truncation returned %d (mapped %d)\n", st, (int)mapped);
+        std::printf("read past a truncation returned %d (mode %d)\n", st, mode);
         return 1;
     }
     if (read_chunk(f, buf.data(), 4096, 0, path, nullptr) != SLLM_OK || std::memcmp(buf.data(), bytes.data(), 4096)) {
@@ -75,14 +79,14 @@ int main(int argc, char** argv) {
     if (argc < 2) return 2;
     const std::string dir = argv[1];
     std::mt19937_64 rng(20261202);
-    for (int mapped = 0; mapped < 2; ++mapped) {
+    for (int mode = 0; mode < 3; ++mode) {
         std::vector<uint8_t> bytes((24u << 20) + 1234);
         for (auto& b : bytes) b = (uint8_t)rng();
-        const std::string path = dir + "/data" + std::to_string(mapped);
+        const std::string path = dir + "/data" + std::to_string(mode);
         FILE* fp = std::fopen(path.c_str(), "wb");
         if (!fp || std::fwrite(bytes.data(), 1, bytes.size(), fp) != bytes.size()) return 1;
         std::fclose(fp);
-        if (check(path, bytes, mapped != 0, rng)) return 1;
+        if (check(path, bytes, mode, rng)) return 1;
     }
     std::printf("ok\n");
     return 0;
