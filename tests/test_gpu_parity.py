@@ -413,9 +413,13 @@ def test_single_hip_runtime(torch_cuda):
 
 @pytest.mark.parametrize("shape", [{"SLLM_K1_UNROLL": "2"}, {"SLLM_K1_UNROLL": "4", "SLLM_K1_NT": "1"},
                                    {"SLLM_K1_BLOCKS": "1024"}, {"SLLM_K1_BLOCKS": "7", "SLLM_K1_UNROLL": "4"},
-                                   {"SLLM_K1_STREAM_BLOCKS": "1"}, {"SLLM_K1_STREAM_BLOCKS": "1024"}])
+                                   {"SLLM_K1_STREAM_BLOCKS": "1"}, {"SLLM_K1_STREAM_BLOCKS": "1024"},
+                                   {"SLLM_SPLIT_CHUNKS": "0"}, {"SLLM_SPLIT_CHUNKS": "1000000"},
+                                   {"SLLM_READ_STREAM": "0"}, {"SLLM_READ_MAPPED": "1", "SLLM_SPLIT_CHUNKS": "1000000"}])
 def test_gather_shapes(torch_cuda, opt125m, shape, monkeypatch):
-    """Every launch shape of the chunk gather gives the same bytes."""
+    """Every launch shape of the chunk gather, and every way the streamed
+    load reads its chunks (whole or in pieces, directly, through the
+    streaming buffer or the mapping), gives the same bytes."""
     for k, v in shape.items():
         monkeypatch.setenv(k, v)
     torch = torch_cuda
