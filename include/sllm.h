@@ -34,6 +34,11 @@
  *     close/destroy call.
  *   - A handle may be used by one thread at a time; different handles may
  *     be used from different threads.
+ *   - Copy streams (and their fork/join events) outlive the handles that
+ *     used them: a closed handle leaves its idle streams to the next handle
+ *     on the same device (at most 32 sets per process, kept until the
+ *     process ends), so opening a handle per load costs no stream creation.
+ *     A caller that resets a device must not use the library afterwards.
  *
  * Environment (read by the library; none is needed for normal use).
  *   SLLM_LOG_LEVEL        0 quiet (default), 1 info, 2 debug, on stderr.
