@@ -253,7 +253,7 @@ int32_t read_chunk(const DataFile& f, void* dst, uint64_t n, uint64_t off, const
         const uint64_t k = n - done < kBounceBytes ? n - done : kBounceBytes;
         int e = pread_exact(f.fd, b, k, off + done);
         if (e) return read_error(e, path, off + done);
-        std::memcpy(d + done, b, k);
+        copy_stream(d + done, b, k);  // streaming stores, as for buffered reads
         done += k;
     }
     if (bounced) *bounced += n;
