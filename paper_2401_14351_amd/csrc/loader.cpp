@@ -165,13 +165,27 @@ bool park_stream_set(sllm_ckpt* h) {
 int32_t ensure_streams(sllm_ckpt* h) {
     if (!h->streams.empty()) return SLLM_OK;
     if (take_stream_set(h->device, h->n_streams, h)) return SLLM_OK;
-    h->streams.assign(h->n_streams, nullptr);
-    h->join_ev.assign(h->n_streams, nullptr);
-    for (uint32_t i = 0; i < h->n_streams; ++i) {
-        SLLM_HIP(hipStreamCreateWithFlags(&h->streams[i], hipStreamNonBlocking));
-        SLLM_HIP(hipEventCreateWithFlags(&h->join_ev[i], hipEventDisableTiming));
+    std::vector<hipStream_t> streams(h->n_streams, nullptr);
+    std::vector<hipEvent_t> join_ev(h->n_streams, nullptr);
+    hipEvent_t fork_ev = nullptr;
+    hipError_t e = hipSuccess;
+    for (uint32_t i = 0; i < h->n_streams && e == hipSuccess; ++i) {
+        e = hipStreamCreateWithFlags(&streams[i], hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&join_ev[i], hipEventDisableTiming);
     }
-    SLLM_HIP(hipEventCreateWithFlags(&h->fork_ev, hipEventDisableTiming));
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&fork_ev, hipEventDisableTiming);
+    if (e != hipSuccess) {
+        // all or nothing: a handle left with a null stream would queue its
+        // copies on the device's null stream at the next load
+        for (hipEvent_t ev : join_ev)
+            if (ev) (void)hipEventDestroy(ev);
+        for (hipStream_t s : streams)
+            if (s) (void)hipStreamDestroy(s);
+        return fail(SLLM_E_HIP, "creating %u copy streams: %s", h->n_streams, hipGetErrorString(e));
+    }
+    h->streams = std::move(streams);
+    h->join_ev = std::move(join_ev);
+    h->fork_ev = fork_ev;
     return SLLM_OK;
 }
 
