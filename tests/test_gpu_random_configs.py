@@ -3,7 +3,12 @@ alignment, device alignment, engine, cached or streamed (buffered or direct
 reads, kept slots), chunk size, ring size and reader count drawn at random,
 every byte of every load (and, with a device alignment, of the HBM repack
 of the file-layout image) compared with the oracle's image and a sentinel
-past it.  Each configuration is printed before it runs."""
+past it.  A second generator draws the library's tuning knobs for each
+configuration (kernel grids and tile shapes, batch target, split reads,
+read mode, copy size, pinned arena size, sometimes a chunk large enough to
+be read in pieces), so that the knobs are exercised in combination; the
+first generator's sequence of configurations does not depend on them.
+Each configuration is printed before it runs."""
 
 import os
 import sys
@@ -18,7 +23,7 @@ pytestmark = pytest.mark.gpu
 
 SENTINEL = 0x3C
 # a longer or different sweep: SLLM_RAND_CONFIGS=5000 SLLM_RAND_SEED=7
-N_CONFIGS = int(os.environ.get("SLLM_RAND_CONFIGS", "600"))
+N_CONFIGS = int(os.environ.get("SLLM_RAND_CONFIGS", "1500"))
 SEED = int(os.environ.get("SLLM_RAND_SEED", "20240114"))
 
 
@@ -58,18 +63,53 @@ def draw(rng):
                 ring=int(rng.integers(1, 9)), io=int(rng.integers(1, 5)))
 
 
-def test_random_configurations(torch_cuda, tmp_path):
+# each knob: values drawn with equal weight, None leaves the default
+KNOBS = {
+    "SLLM_K1_BLOCKS": [None, None, "1", "3", "2048"],
+    "SLLM_K1_STREAM_BLOCKS": [None, None, "1", "5", "1024"],
+    "SLLM_K1_UNROLL": [None, None, "1", "2"],
+    "SLLM_K1_NT": [None, "1"],
+    "SLLM_K2_NT": [None, "0"],
+    "SLLM_K2_UNROLL": [None, "4"],
+    "SLLM_K2_MAX_GRID": [None, None, "7", "997"],
+    "SLLM_BATCH_TARGET_MB": [None, "0", "1"],
+    "SLLM_SPLIT_CHUNKS": [None, "0", "1", "1000"],
+    "SLLM_READ_STREAM": [None, "0"],
+    "SLLM_READ_MAPPED": [None, None, "1"],
+    "SLLM_SDMA_MAX_COPY_MB": [None, "1"],
+    "SLLM_POOL_ARENA_MB": [None, None, "1", "3"],
+}
+
+
+def draw_knobs(rng):
+    env = {}
+    for name, values in KNOBS.items():
+        v = values[int(rng.integers(0, len(values)))]
+        if v is not None:
+            env[name] = v
+    # sometimes chunks of 2-5 MiB, which the first readers take in pieces
+    big_chunk = 4096 * int(rng.integers(512, 1281)) if rng.integers(0, 4) == 0 else 0
+    return env, big_chunk
+
+
+def test_random_configurations(torch_cuda, tmp_path, monkeypatch):
     torch = torch_cuda
     rng = np.random.default_rng(SEED)
+    knob_rng = np.random.default_rng(SEED + 1)
     for i in range(N_CONFIGS):
         cfg = draw(rng)
+        env, big_chunk = draw_knobs(knob_rng)
         spec = cfg.pop("spec")
-        say(i, cfg)
+        say(i, cfg, env, "big chunk" if big_chunk else "")
+        for name in KNOBS:
+            monkeypatch.delenv(name, raising=False)
+        for name, v in env.items():
+            monkeypatch.setenv(name, v)
         tensors = [(t.name, t.dtype, t.shape, d) for t, d in zip(spec.tensors, synth.materialize(spec, threads=4))]
         A, A2 = cfg["A"], cfg["A2"]
         # at most 2048 chunks (every pool chunk takes at least 4 KiB of pinned memory)
         _, T = oracle.plan_layout([t.nbytes for t in spec.tensors], A)
-        C = max(cfg["C"], -(-T // 2048))
+        C = max(big_chunk or cfg["C"], -(-T // 2048))
         if cfg["source"] == "direct":
             C = -(-C // 4096) * 4096
         cfg["C"] = C
