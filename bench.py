@@ -297,12 +297,22 @@ def cpu_baseline(d: str, budget_s: float):
             if dt >= budget_s / 2 or k == n_all:
                 break
             k = min(n_all, max(k + 1, int(k * min(8.0, budget_s / 2 / max(dt, 1e-3)))))
+        # a whole file that reads faster than that: time several passes over it
+        passes = 1
+        if k == n_all and dt < budget_s / 2:
+            passes = 0
+            t0 = time.perf_counter()
+            while passes < 2 or time.perf_counter() - t0 < budget_s * 0.7:
+                oracle.read(d, C, max_chunks=k)
+                passes += 1
+            dt = time.perf_counter() - t0
     finally:
         os.sched_setaffinity(0, prev)
-    nbytes = min(k * C, index.total_bytes)
+    nbytes = min(k * C, index.total_bytes) * passes
+    what = f"first {k} of {n_all} chunks" if passes == 1 else f"{passes} passes over all {n_all} chunks"
     return {"value": round(nbytes / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"oracle chunked reader (file -> host buffer, page cache warm), first {k} of {n_all} "
-                      f"chunks ({nbytes / 1e9:.2f} GB) in {dt:.1f} s on one core",
+            "sample": f"oracle chunked reader (file -> host buffer, page cache warm), {what} "
+                      f"({nbytes / 1e9:.2f} GB) in {dt:.1f} s on one core",
             "host": host_info()}
 
 
