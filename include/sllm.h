@@ -39,6 +39,10 @@
  *     on the same device (at most 32 sets per process, kept until the
  *     process ends), so opening a handle per load costs no stream creation.
  *     A caller that resets a device must not use the library afterwards.
+ *   - Reader threads outlive the loads that start them: a finished reader
+ *     waits idle (at most 64 per process, until the process ends) for the
+ *     next load or pool fill, which then wakes it instead of starting a
+ *     thread.
  *
  * Environment (read by the library; none is needed for normal use).
  *   SLLM_LOG_LEVEL        0 quiet (default), 1 info, 2 debug, on stderr.
@@ -53,6 +57,11 @@
  *   SLLM_READ_MAPPED=1    buffered files are mapped and chunks copied with
  *                         streaming stores instead of read with pread.
  *   SLLM_BATCH_TARGET_MB  bytes a streamed gather batch collects (64).
+ *   SLLM_SPLIT_CHUNKS     leading chunks of a streamed load that all readers
+ *                         read together in pieces (one per I/O thread; 0
+ *                         reads every chunk whole).
+ *   SLLM_IDLE_WORKERS     idle reader threads kept for later loads (64; 0
+ *                         starts every reader on a new thread).
  *   SLLM_SDMA_MAX_COPY_MB largest merged copy-engine copy of cached chunks (256).
  *   SLLM_POOL_ARENA_MB    size of each pinned allocation a pool is cut from (1024).
  *   SLLM_K1_BLOCKS, SLLM_K1_STREAM_BLOCKS, SLLM_K1_UNROLL, SLLM_K1_NT,

@@ -12,6 +12,7 @@
 #include <thread>
 
 #include "common.hpp"
+#include "workers.hpp"
 
 namespace sllm {
 
@@ -174,19 +175,17 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
     };
 
 
-    std::vector<std::thread> threads;
-    try {
-        threads.reserve(nt);
-        for (uint32_t i = 0; i < nt; ++i) threads.emplace_back(reader, i);
-    } catch (...) {  // could not start every reader: stop the ones that run
+    TaskGroup readers;  // idle threads of earlier loads, else new ones
+    if (readers.start(nt, reader) != SLLM_OK) {  // could not start every reader: stop the ones that run
+        const std::string why = sllm_last_error();
         {
             std::lock_guard<std::mutex> g(mu);
             stop = true;
             cv_free.notify_all();
         }
-        for (auto& t : threads) t.join();
+        readers.wait();
         sink.drain();
-        return fail(SLLM_E_NOMEM, "cannot start %u I/O threads", nt);
+        return fail(SLLM_E_NOMEM, "cannot start %u I/O threads: %s", nt, why.c_str());
     }
 
     // give the slots of completed batches back to the readers; with `block`,
@@ -287,7 +286,7 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         stop = true;
         cv_free.notify_all();
     }
-    for (auto& t : threads) t.join();
+    readers.wait();
     if (stats) {
         stats->t_start = t_start;
         stats->bytes_read = bytes_read;

@@ -16,6 +16,7 @@
 #include <thread>
 
 #include "hip_util.hpp"
+#include "workers.hpp"
 
 using namespace sllm;
 
@@ -97,13 +98,14 @@ int32_t parallel_chunks(uint64_t n, uint32_t threads, const std::function<int32_
         }
     };
     uint32_t nt = (uint32_t)std::min<uint64_t>(threads ? threads : 1, n ? n : 1);
-    std::vector<std::thread> pool;
-    try {
-        for (uint32_t i = 1; i < nt; ++i) pool.emplace_back(worker);
-    } catch (...) {  // fewer threads than asked: the ones running finish the work
+    {
+        // the caller is one of the workers; fewer threads than asked is fine
+        // (the ones running finish the work)
+        TaskGroup helpers;
+        if (nt > 1 && helpers.start(nt - 1, [&](uint32_t) { worker(); }) != SLLM_OK) clear_error();
+        worker();
+        helpers.wait();
     }
-    worker();
-    for (auto& t : pool) t.join();
     if (status.load() != SLLM_OK) return fail(status.load(), "%s", msg.c_str());
     return SLLM_OK;
 }

@@ -30,6 +30,7 @@
 
 #include "common.hpp"
 #include "pipeline.hpp"
+#include "workers.hpp"
 
 using namespace sllm;
 
@@ -449,9 +450,47 @@ void random_split(Case& cs, std::mt19937_64& rng) {
     cs.split_align = aligns[rng() % 4];
 }
 
+// Task groups started from several threads at once, as concurrent loads
+// start their readers: every task runs exactly once, on a thread of its own
+// (all of a group's tasks run at the same time: each waits for the others),
+// and the idle list never exceeds its bound.
+int check_task_groups(int rounds) {
+    std::atomic<int> bad{0};
+    auto client = [&](uint64_t seed) {
+        std::mt19937_64 rng(seed);
+        for (int r = 0; r < rounds; ++r) {
+            const uint32_t n = 1 + (uint32_t)(rng() % 24);
+            std::vector<std::atomic<int>> ran(n);
+            for (auto& x : ran) x = 0;
+            std::mutex mu;
+            std::condition_variable cv;
+            uint32_t arrived = 0;
+            TaskGroup g;
+            const int32_t st = g.start(n, [&](uint32_t i) {
+                ran[i].fetch_add(1);
+                std::unique_lock<std::mutex> lk(mu);
+                if (++arrived == n) cv.notify_all();
+                // a barrier: only threads of their own can all get past it
+                if (!cv.wait_for(lk, std::chrono::seconds(20), [&] { return arrived == n; })) bad.fetch_add(1);
+            });
+            g.wait();
+            if (st != SLLM_OK || g.started() != n) bad.fetch_add(1);
+            for (auto& x : ran)
+                if (x.load() != 1) bad.fetch_add(1);
+            if (idle_workers() > kMaxIdleWorkers) bad.fetch_add(1);
+        }
+    };
+    std::vector<std::thread> clients;
+    for (uint64_t c = 0; c < 4; ++c) clients.emplace_back(client, 77 + c);
+    for (auto& t : clients) t.join();
+    if (bad.load()) std::printf("task groups: %d failures\n", bad.load());
+    return bad.load() ? 1 : 0;
+}
+
 int main(int argc, char** argv) {
     const int n_cases = argc > 1 ? std::atoi(argv[1]) : 300;
     std::mt19937_64 rng(20240114351ull);
+    if (check_task_groups(n_cases) != 0) return 1;
     const uint64_t Cs[] = {1, 7, 16, 64, 100, 4096};
     int failures = 0;
     for (int i = 0; i < n_cases; ++i) {

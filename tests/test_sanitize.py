@@ -33,7 +33,7 @@ def test_format_code_under_sanitizers(tmp_path):
     assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, r.stderr
 
 
-PIPELINE_SOURCES = ["common.cpp", "pipeline.cpp"]
+PIPELINE_SOURCES = ["common.cpp", "pipeline.cpp", "workers.cpp"]
 # clang's ThreadSanitizer: the one in GCC 11 does not intercept
 # pthread_cond_clockwait, which std::condition_variable::wait_for uses, and
 # then reports false races on every mutex it waits with.
