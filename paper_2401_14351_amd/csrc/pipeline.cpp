@@ -187,6 +187,16 @@ int32_t run_stream(const StreamPlan& p, const ChunkReader& read, BatchSink& sink
         sink.drain();
         return fail(SLLM_E_NOMEM, "cannot start %u I/O threads: %s", nt, why.c_str());
     }
+    // however this function ends (an exception included), stop the readers
+    // before `readers` waits for them, so that none stays blocked on a slot
+    struct StopReaders {
+        std::function<void()> f;
+        ~StopReaders() { f(); }
+    } stop_readers{[&] {
+        std::lock_guard<std::mutex> g(mu);
+        stop = true;
+        cv_free.notify_all();
+    }};
 
     // give the slots of completed batches back to the readers; with `block`,
     // wait for the oldest batch first

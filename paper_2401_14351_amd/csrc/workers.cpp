@@ -109,6 +109,7 @@ TaskGroup::TaskGroup() : st_(std::make_shared<State>()) {}
 TaskGroup::~TaskGroup() { wait(); }
 
 int32_t TaskGroup::start(uint32_t n, std::function<void(uint32_t)> fn) {
+    if (started_) return fail(SLLM_E_INVAL, "a task group is started once");
     st_->fn = std::move(fn);
     for (uint32_t i = 0; i < n; ++i) {
         {

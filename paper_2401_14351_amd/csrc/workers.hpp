@@ -26,9 +26,9 @@ class TaskGroup {
     TaskGroup& operator=(const TaskGroup&) = delete;
     ~TaskGroup();
 
-    // Start fn(i) for i in [0, n).  SLLM_E_NOMEM if a thread could not be
-    // started; the tasks started before it keep running (started() of them)
-    // and wait() still waits for them.
+    // Start fn(i) for i in [0, n); once per group.  SLLM_E_NOMEM if a thread
+    // could not be started; the tasks started before it keep running
+    // (started() of them) and wait() still waits for them.
     int32_t start(uint32_t n, std::function<void(uint32_t)> fn);
     uint32_t started() const { return started_; }
     void wait();
