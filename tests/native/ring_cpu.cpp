@@ -182,11 +182,12 @@ struct Case {
     uint64_t target;
     bool keep;
     uint64_t split_chunks = 0, split_min = 1, split_align = 1;  // leading chunks read in pieces
+    uint64_t tail = 0;  // reads reach tail bytes past T (a direct read's padded end)
 };
 
 // A piece must lie inside its chunk and start at a multiple of the alignment.
 void check_piece(const Case& cs, uint64_t k, uint64_t off, uint64_t len) {
-    const uint64_t chunk_len = std::min(cs.C, cs.T - k * cs.C);
+    const uint64_t chunk_len = std::min(cs.C, cs.T + cs.tail - k * cs.C);
     if (off + len > chunk_len || (off % cs.split_align) != 0 || (off && k >= cs.split_chunks)) ++g_violations;
 }
 
@@ -195,8 +196,8 @@ void check_piece(const Case& cs, uint64_t k, uint64_t off, uint64_t len) {
 int run_case(const Case& cs, uint64_t seed, int inject) {
     std::mt19937_64 rng(seed);
     const uint64_t n = ceil_div(cs.T, cs.C);
-    std::vector<uint8_t> file(cs.T);
-    for (auto& b : file) b = (uint8_t)rng();
+    std::vector<uint8_t> file(cs.T + cs.tail, 0);  // zero past T, as a padded file
+    for (uint64_t i = 0; i < cs.T; ++i) file[i] = (uint8_t)rng();
     const uint32_t n_slots = cs.keep ? (uint32_t)std::max<uint64_t>(n, 1) : cs.slots;
     std::vector<uint8_t> slots((uint64_t)n_slots * cs.C);
     std::vector<uint8_t> dst(cs.T);
@@ -222,7 +223,7 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
     StreamPlan plan;
     plan.chunk = cs.C;
     plan.total = cs.T;
-    plan.read_end = cs.T;
+    plan.read_end = cs.T + cs.tail;
     plan.io_threads = cs.threads;
     plan.n_slots = n_slots;
     plan.max_batch = cs.max_batch;
@@ -278,8 +279,9 @@ int run_case(const Case& cs, uint64_t seed, int inject) {
                 return 1;
             }
         }
-        if (ss.bytes_read != cs.T) {
-            std::printf("read %llu bytes of %llu\n", (unsigned long long)ss.bytes_read, (unsigned long long)cs.T);
+        const uint64_t want_read = std::min(cs.T + cs.tail, n * cs.C);
+        if (ss.bytes_read != want_read) {
+            std::printf("read %llu bytes of %llu\n", (unsigned long long)ss.bytes_read, (unsigned long long)want_read);
             return 1;
         }
         if (cs.T && std::memcmp(dst.data(), file.data(), cs.T) != 0) {
@@ -503,13 +505,15 @@ int main(int argc, char** argv) {
         cs.target = 1 + rng() % 4;
         cs.keep = rng() % 5 == 0;
         random_split(cs, rng);
+        cs.tail = rng() % 4 == 0 ? rng() % (cs.C + 1) : 0;
         const int inject = (int)(i % 3);  // none, read error, move error
         if (run_case(cs, rng(), inject) != 0) {
             std::printf("case %d failed: T=%llu C=%llu slots=%u threads=%u max_batch=%u target=%llu keep=%d inject=%d "
-                        "split=%llu/%llu/%llu\n",
+                        "split=%llu/%llu/%llu tail=%llu\n",
                         i, (unsigned long long)cs.T, (unsigned long long)cs.C, cs.slots, cs.threads, cs.max_batch,
                         (unsigned long long)cs.target, (int)cs.keep, inject, (unsigned long long)cs.split_chunks,
-                        (unsigned long long)cs.split_min, (unsigned long long)cs.split_align);
+                        (unsigned long long)cs.split_min, (unsigned long long)cs.split_align,
+                        (unsigned long long)cs.tail);
             ++failures;
             if (failures > 5) break;
         }
