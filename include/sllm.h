@@ -459,8 +459,11 @@ int32_t sllm_estimator_complete_load(sllm_estimator* e, uint64_t task, const sll
 /* Current bandwidth estimate of one tier (bytes per second).  Errors: INVAL. */
 int32_t sllm_estimator_bandwidth(const sllm_estimator* e, uint32_t tier, double* bytes_per_s);
 
-/* Close the handle; waits for its in-flight device work first.  NULL is a
- * no-op.  Errors: BUSY (a load is running on the handle). */
+/* Close the handle; waits for its in-flight device work first (the copy
+ * streams' and, on the caller's streams, that of every load and repack the
+ * handle enqueued), so that the pool chunks and device tables that work
+ * reads may be reused as soon as it returns.  NULL is a no-op.
+ * Errors: BUSY (a load is running on the handle). */
 int32_t sllm_close(sllm_ckpt* h);
 
 /* Message of the last failed call on this thread ("" if none). */

@@ -62,6 +62,12 @@ struct sllm_ckpt {
     std::vector<hipStream_t> streams;
     std::vector<hipEvent_t> join_ev;
     hipEvent_t fork_ev = nullptr, t0_ev = nullptr, t1_ev = nullptr;
+    // recorded on the caller's stream after each load or repack, so that
+    // close waits for device work that ran on such a stream alone (a cached
+    // kernel-engine load, a repack) before the pool chunks and tables it
+    // reads go back: the events of loads and repacks that may still run, and
+    // completed ones for reuse
+    mutable std::vector<hipEvent_t> end_evs, end_free;
     bool timed = false;             // t0/t1 bracket the last load
     DeviceLayout layout;            // device tables for A2 layouts
     bool keep = false;              // SLLM_OPEN_CACHE: chunk k streams into slot k, kept afterwards
@@ -96,9 +102,12 @@ bool park_stream_set(sllm_ckpt* h);
 
 void release(sllm_ckpt* h) {
     const bool used_hip = !h->streams.empty() || !h->slots.empty() || h->fork_ev || h->t0_ev || h->t1_ev ||
-                          h->layout.d_off || h->layout.staging;
+                          !h->end_evs.empty() || !h->end_free.empty() || h->layout.d_off || h->layout.staging;
     if (used_hip) {
         DeviceGuard guard(h->device);
+        for (hipEvent_t e : h->end_evs) (void)hipEventSynchronize(e);
+        for (hipEvent_t e : h->end_evs) (void)hipEventDestroy(e);
+        for (hipEvent_t e : h->end_free) (void)hipEventDestroy(e);
         for (hipStream_t s : h->streams)
             if (s) (void)hipStreamSynchronize(s);
         for (const InFlightBatch& b : h->inflight) (void)hipEventSynchronize(h->slots[b.token].done);
@@ -186,6 +195,32 @@ int32_t ensure_streams(sllm_ckpt* h) {
     h->streams = std::move(streams);
     h->join_ev = std::move(join_ev);
     h->fork_ev = fork_ev;
+    return SLLM_OK;
+}
+
+// Record an end event on `s` after a load's or repack's work (events of
+// earlier ones that have completed are reused).
+int32_t mark_end(const sllm_ckpt* h, hipStream_t s) {
+    for (size_t i = 0; i < h->end_evs.size();) {
+        if (hipEventQuery(h->end_evs[i]) == hipSuccess) {
+            h->end_free.push_back(h->end_evs[i]);
+            h->end_evs[i] = h->end_evs.back();
+            h->end_evs.pop_back();
+        } else {
+            ++i;
+        }
+    }
+    (void)hipGetLastError();  // a query of pending work is not an error
+    hipEvent_t e = nullptr;
+    if (!h->end_free.empty()) {
+        e = h->end_free.back();
+    } else {
+        SLLM_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+        h->end_free.push_back(e);
+    }
+    SLLM_HIP(hipEventRecord(e, s));
+    h->end_free.pop_back();
+    h->end_evs.push_back(e);
     return SLLM_OK;
 }
 
@@ -722,6 +757,13 @@ extern "C" int32_t sllm_load(sllm_ckpt* h, void* dev_dst, uint64_t dst_bytes, vo
         (void)hipStreamSynchronize(user);
         return st;
     }
+    if (h->dev_total) {
+        st = mark_end(h, user);
+        if (st != SLLM_OK) {
+            (void)hipStreamSynchronize(user);
+            return st;
+        }
+    }
     if (timing) {
         SLLM_HIP(hipEventRecord(h->t1_ev, user));
         h->timed = true;
@@ -753,8 +795,9 @@ extern "C" int32_t sllm_repack(const sllm_ckpt* h, const void* src_dev, uint64_t
     SLLM_TRY(check_device_range(dst_dev, h->dev_total, h->device, "destination"));
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint8_t* dst = static_cast<uint8_t*>(dst_dev);
-    return launch_scatter_window(h->layout, dst, static_cast<const uint8_t*>(src_dev), 0, h->ix.total,
-                                 /*src_is_host=*/false, s);
+    SLLM_TRY(launch_scatter_window(h->layout, dst, static_cast<const uint8_t*>(src_dev), 0, h->ix.total,
+                                   /*src_is_host=*/false, s));
+    return mark_end(h, s);
 } SLLM_CATCH_ALL
 
 extern "C" int32_t sllm_repack_noalloc(const sllm_ckpt* h, uint64_t dev_alignment, const void* src_dev,
