@@ -717,3 +717,58 @@ def test_mapped_reader(torch_cuda, opt125m, engine, monkeypatch, tmp_path):
         with open(path, "wb") as f:
             f.write(full)
         assert_same(run_load(torch, ck, len(want)), want, "mapped, after restoring the file")
+
+
+@pytest.mark.parametrize("engine", ["kernel", "sdma"])
+@pytest.mark.parametrize("A2", [0, 256])
+@pytest.mark.parametrize("cached", [False, True])
+def test_load_into_a_region_of_an_arena(torch_cuda, tmp_path, engine, A2, cached):
+    """The destination is a region inside a larger device allocation (a
+    serving arena): the load writes exactly that region, every byte equal to
+    the oracle's, nothing before or after it; views built over the region
+    hold each tensor's bytes; a region that is not 16-byte aligned, or one
+    byte short, is refused before any device work."""
+    torch = torch_cuda
+    spec = synth.tiny(21, n=20, alignment=256, max_bytes=50_000)
+    tensors = tensors_of(spec)
+    d = str(tmp_path / "arena")
+    binding.convert(iter(tensors), d, 256, 4096)
+    want, index = expected(tensors, 256, A2)
+    pool = binding.Pool(4096, -(-index.total_bytes // 4096)) if cached else None
+    try:
+        if pool:
+            pool.cache(d)
+        with binding.Checkpoint(d, pool=pool, engine=engine, dev_alignment=A2, ring_slots=4) as ck:
+            s = torch.cuda.Stream()
+            for start in (16, 48, 4096 + 16):
+                say("arena region", engine, A2, cached, start)
+                arena = torch.full((start + len(want) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+                region = arena[start:start + len(want)]
+                s.wait_stream(torch.cuda.current_stream())
+                ck.load_into(region, s)
+                s.synchronize()
+                host = arena.cpu().numpy()
+                assert (host[:start] == SENTINEL).all(), f"bytes before the region written (start {start})"
+                assert (host[start + len(want):] == SENTINEL).all(), f"bytes after the region written (start {start})"
+                assert_same(host[start:start + len(want)].tobytes(), want, f"region at {start}")
+                region.fill_(SENTINEL)
+                views = ck.load_with_views(region, s)
+                s.synchronize()
+                for (name, dt, shape, data) in tensors:
+                    v = views[name]
+                    assert tuple(v.shape) == tuple(shape), name
+                    got = v.reshape(-1).contiguous().view(torch.uint8).cpu().numpy().tobytes()  # 0-d: one element
+                    assert got == data.tobytes(), name
+            arena = torch.full((len(want) + 64,), SENTINEL, dtype=torch.uint8, device="cuda:0")
+            with pytest.raises(binding.SllmError) as e:  # 8-byte aligned only
+                ck.load(arena.data_ptr() + 8, len(want), s)
+            assert e.value.code == -1
+            with pytest.raises(binding.SllmError) as e:  # a region one byte short
+                ck.load(arena.data_ptr() + 16, len(want) - 1, s)
+            assert e.value.code == -6
+            torch.cuda.synchronize()
+            assert (arena.cpu().numpy() == SENTINEL).all(), "a refused load wrote bytes"
+    finally:
+        if pool:
+            pool.evict(d)
+            pool.close()
