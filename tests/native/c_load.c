@@ -3,7 +3,8 @@
  * open a converted checkpoint, load it into hipMalloc'd memory with both
  * engines (cached in a pool and streamed from the file, file layout and a
  * 256-byte device layout), copy the image back and compare it with the
- * expected bytes, and look tensors up through the index.
+ * expected bytes, look tensors up through the index, and check that
+ * destinations outside one device allocation are refused.
  *
  *   c_load <checkpoint dir> <expected file image> <expected A2=256 image> <chunk size>
  *
@@ -97,6 +98,57 @@ static int load_and_compare(const char* dir, sllm_pool* pool, uint32_t engine, u
     return 0;
 }
 
+/* Destinations the load must refuse before any device work: a range that
+ * runs 16 bytes past the end of its allocation (as the runtime reports the
+ * allocation), fewer bytes than the image, an address that is not 16-byte
+ * aligned, and host memory.  The allocation keeps its fill byte throughout;
+ * then a load into the allocation's last `total` bytes succeeds. */
+static int refusals(const char* dir, uint64_t chunk, const unsigned char* want, size_t want_n) {
+    sllm_open_opts o;
+    memset(&o, 0, sizeof o);
+    o.chunk_size = chunk;
+    o.ring_slots = 3;
+    o.io_threads = 2;
+    sllm_ckpt* h = NULL;
+    CHECK(sllm_open(dir, &o, &h) == SLLM_OK, "sllm_open: %s", sllm_last_error());
+    const uint64_t total = sllm_total_bytes(h);
+    CHECK(total == want_n && total > 0, "total %llu", (unsigned long long)total);
+    const size_t alloc = (size_t)total + 4096;
+    unsigned char* dev = NULL;
+    CHECK(hipMalloc((void**)&dev, alloc) == hipSuccess, "hipMalloc");
+    CHECK(hipMemset(dev, 0x5A, alloc) == hipSuccess, "hipMemset");
+    CHECK(hipDeviceSynchronize() == hipSuccess, "hipDeviceSynchronize");
+    void* base = NULL;
+    size_t size = 0;
+    CHECK(hipMemGetAddressRange(&base, &size, dev) == hipSuccess && base == dev && size >= alloc,
+          "hipMemGetAddressRange");
+    /* 16-byte aligned, ending 1-16 bytes past what the runtime counts as the allocation */
+    const size_t over_off = ((size - total) / 16 + 1) * 16;
+    unsigned char* over = (unsigned char*)base + over_off;
+    CHECK(sllm_load(h, over, total, NULL) == SLLM_E_RANGE, "load past the allocation: %s", sllm_last_error());
+    CHECK(sllm_load(h, dev, total - 1, NULL) == SLLM_E_RANGE, "short destination accepted");
+    CHECK(sllm_load(h, dev + 8, total, NULL) == SLLM_E_INVAL, "unaligned destination accepted");
+    unsigned char* host = (unsigned char*)malloc(total);
+    CHECK(host != NULL, "malloc");
+    CHECK(sllm_load(h, host, total, NULL) == SLLM_E_INVAL, "host destination accepted");
+    CHECK(hipDeviceSynchronize() == hipSuccess, "hipDeviceSynchronize");
+    unsigned char* back = (unsigned char*)malloc(alloc);
+    CHECK(back != NULL, "malloc");
+    CHECK(hipMemcpy(back, dev, alloc, hipMemcpyDeviceToHost) == hipSuccess, "hipMemcpy");
+    for (size_t i = 0; i < alloc; ++i) CHECK(back[i] == 0x5A, "a refused load wrote byte %zu", i);
+    /* the allocation's last `total` bytes (16-byte aligned as `alloc - total` is) */
+    CHECK(sllm_load(h, dev + alloc - total, total, NULL) == SLLM_OK, "load at the end: %s", sllm_last_error());
+    CHECK(hipDeviceSynchronize() == hipSuccess, "hipDeviceSynchronize");
+    CHECK(hipMemcpy(back, dev, alloc, hipMemcpyDeviceToHost) == hipSuccess, "hipMemcpy");
+    CHECK(memcmp(back + alloc - total, want, total) == 0, "load at the end: image differs");
+    for (size_t i = 0; i < alloc - total; ++i) CHECK(back[i] == 0x5A, "byte %zu before the image written", i);
+    free(back);
+    free(host);
+    CHECK(hipFree(dev) == hipSuccess, "hipFree");
+    CHECK(sllm_close(h) == SLLM_OK, "sllm_close: %s", sllm_last_error());
+    return 0;
+}
+
 int main(int argc, char** argv) {
     if (argc != 5) {
         printf("usage: c_load <dir> <expected image> <expected A2=256 image> <chunk size>\n");
@@ -124,6 +176,9 @@ int main(int argc, char** argv) {
         printf("engine %u ok\n", engines[e]);
         fflush(stdout);
     }
+    if (refusals(dir, chunk, want1, n1)) return 1;
+    printf("refusals ok\n");
+    fflush(stdout);
     CHECK(sllm_pool_evict(pool, dir) == SLLM_OK, "sllm_pool_evict: %s", sllm_last_error());
     CHECK(sllm_pool_destroy(pool) == SLLM_OK, "sllm_pool_destroy: %s", sllm_last_error());
     free(want1);
