@@ -1,5 +1,7 @@
 #include "workers.hpp"
 
+#include <pthread.h>
+
 #include <cstdlib>
 #include <thread>
 #include <utility>
@@ -26,8 +28,26 @@ struct Registry {
     std::mutex mu;
     std::vector<Worker*> idle;
 };
+Registry& registry();
+
+// A child of fork() has only the thread that forked: the idle threads of the
+// list do not exist there, so the child forgets them (their Worker records
+// leak) and starts new threads when it needs some.  The list's lock is held
+// across fork so that the child never inherits it locked.
+void before_fork() { registry().mu.lock(); }
+void after_fork_parent() { registry().mu.unlock(); }
+void after_fork_child() {
+    Registry& r = registry();
+    r.idle.clear();
+    r.mu.unlock();
+}
+
 Registry& registry() {
-    static Registry* r = new Registry;
+    static Registry* r = [] {
+        auto* reg = new Registry;
+        (void)pthread_atfork(before_fork, after_fork_parent, after_fork_child);
+        return reg;
+    }();
     return *r;
 }
 

@@ -90,3 +90,18 @@ def test_chunk_reader_under_sanitizers(tmp_path):
     assert r.returncode == 0, r.stdout + r.stderr
     assert r.stdout.strip() == "ok", r.stdout
     assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, r.stderr
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ not available")
+def test_kept_threads_across_fork(tmp_path):
+    """A child of fork() starts threads of its own instead of handing tasks
+    to the parent's idle ones, which do not exist in the child."""
+    exe = tmp_path / "workers_fork"
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", f"-I{ROOT}/include", f"-I{CSRC}",
+           os.path.join(ROOT, "tests", "native", "workers_fork.cpp"),
+           *[os.path.join(CSRC, s) for s in ("common.cpp", "workers.cpp")], "-o", str(exe), "-lpthread"]
+    subprocess.run(cmd, check=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
+    r = subprocess.run([str(exe)], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr
