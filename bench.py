@@ -22,6 +22,7 @@ import argparse
 import hashlib
 import json
 import os
+import shutil
 import statistics
 import sys
 import time
@@ -83,6 +84,54 @@ def spec_key(spec) -> str:
     for t in spec.tensors:
         h.update(f"{t.name}:{t.dtype}:{t.shape}:{t.init};".encode())
     return h.hexdigest()[:16]
+
+
+BENCH_BASES = ("/tmp/sllm_bench", "/dev/shm/sllm_bench")
+
+
+def _free_bytes(path: str) -> int:
+    """Free bytes of the file system that holds `path` (or its nearest
+    existing parent)."""
+    while path and not os.path.exists(path):
+        path = os.path.dirname(path)
+    try:
+        return shutil.disk_usage(path or "/").free
+    except OSError:
+        return 0
+
+
+def checkpoint_dir(spec) -> str:
+    """Where the converted workload lives: under $SLLM_BENCH_DIR if set;
+    else where a converted copy already is; else the first of /tmp and
+    /dev/shm whose file system has room for it (an upper bound: payload plus
+    a full alignment per tensor plus the 4 KiB tail, and 1 GiB to spare), so
+    that a small local disk does not stop the larger workloads."""
+    env = os.environ.get("SLLM_BENCH_DIR")
+    if env:
+        return os.path.join(env, spec.name)
+    key = spec_key(spec)
+    for base in BENCH_BASES:
+        marker = os.path.join(base, spec.name, "bench.key")
+        if os.path.exists(marker) and open(marker).read() == key:
+            return os.path.join(base, spec.name)
+    need = spec.payload_bytes + len(spec.tensors) * spec.alignment + 4096 + (1 << 30)
+    for base in BENCH_BASES:
+        d = os.path.join(base, spec.name)
+        # a partial copy of this workload there will be overwritten: count it as free
+        have = _free_bytes(base) + (_dir_bytes(d) if os.path.isdir(d) else 0)
+        if have >= need:
+            return d
+    return os.path.join(BENCH_BASES[0], spec.name)  # the write reports what is missing
+
+
+def _dir_bytes(d: str) -> int:
+    total = 0
+    for f in os.listdir(d):
+        try:
+            total += os.path.getsize(os.path.join(d, f))
+        except OSError:
+            pass
+    return total
 
 
 def ensure_checkpoint(spec, d: str):
@@ -637,7 +686,7 @@ def measure_k2(torch, workload: str, dev_alignment: int, stream, reps: int = 6, 
     timed with HIP events on the stream K2 runs on; then every byte of the
     result is checked against the generator's bytes."""
     spec = synth.config(workload)
-    d = os.path.join(os.environ.get("SLLM_BENCH_DIR", "/tmp/sllm_bench"), spec.name)
+    d = checkpoint_dir(spec)
     digests = ensure_checkpoint(spec, d)
     with binding.Checkpoint(d, index_only=True) as ck:
         T, file_off = ck.total_bytes, [t.offset for t in ck.tensors()]
@@ -860,7 +909,7 @@ def main():
         return
 
     spec = synth.config(args.workload)
-    d = args.dir or os.path.join(os.environ.get("SLLM_BENCH_DIR", "/tmp/sllm_bench"), spec.name)
+    d = args.dir or checkpoint_dir(spec)
     digests = ensure_checkpoint(spec, d)
     cpu = None if args.no_cpu_baseline else cpu_baseline(d, args.cpu_budget)  # before any GPU work
     if cpu:

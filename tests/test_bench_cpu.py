@@ -1,7 +1,7 @@
 """Host-side arithmetic of bench.py that needs no GPU: the PCI Express
 capability decoding behind the link ceiling, the ceiling itself, and the
 share of the repack kernel's tiles on each path (checked against a per-tile
-brute force over small layouts)."""
+brute force over small layouts), and where a converted workload is kept."""
 
 import os
 import random
@@ -89,3 +89,32 @@ def test_k2_tile_paths_against_brute_force(A, A2):
         tiles, straight, shifted = _tile_paths_brute(file_off, dev_off, sizes, T2)
         assert (got["tiles"], got["straight"], got["shifted"]) == (tiles, straight, shifted)
         assert got["general"] == tiles - straight - shifted
+
+
+def test_checkpoint_dir_choice(tmp_path, monkeypatch):
+    """Where the bench and the full-size tests keep a converted workload:
+    $SLLM_BENCH_DIR when set; else a directory that already holds a
+    converted copy with the right key; else the first base whose file
+    system has room (payload + a full alignment per tensor + 4 KiB + 1 GiB);
+    else the first base, where the write reports the shortage."""
+    from paper_2401_14351_amd import synth
+
+    spec = synth.config("opt-125m")
+    need = spec.payload_bytes + len(spec.tensors) * spec.alignment + 4096 + (1 << 30)
+    a, b = str(tmp_path / "disk"), str(tmp_path / "shm")
+    monkeypatch.setattr(bench, "BENCH_BASES", (a, b))
+    monkeypatch.delenv("SLLM_BENCH_DIR", raising=False)
+    free = {a: need, b: need}
+    monkeypatch.setattr(bench, "_free_bytes", lambda p: free[p])
+    assert bench.checkpoint_dir(spec) == os.path.join(a, spec.name)
+    free[a] = need - 1
+    assert bench.checkpoint_dir(spec) == os.path.join(b, spec.name)
+    free[b] = 0
+    assert bench.checkpoint_dir(spec) == os.path.join(a, spec.name)
+    # a converted copy is used wherever it is, whatever the free space
+    os.makedirs(os.path.join(b, spec.name))
+    with open(os.path.join(b, spec.name, "bench.key"), "w") as f:
+        f.write(bench.spec_key(spec))
+    assert bench.checkpoint_dir(spec) == os.path.join(b, spec.name)
+    monkeypatch.setenv("SLLM_BENCH_DIR", str(tmp_path / "env"))
+    assert bench.checkpoint_dir(spec) == str(tmp_path / "env" / spec.name)

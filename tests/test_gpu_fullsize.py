@@ -45,7 +45,8 @@ def converted(spec, d=None):
         sys.path.insert(0, ROOT)
     import bench
 
-    d = d or os.path.join(os.environ.get("SLLM_BENCH_DIR", "/tmp/sllm_bench"), spec.name)
+    d = d or bench.checkpoint_dir(spec)
+    say(f"{spec.name}: converted checkpoint in {d}")
     return d, bench.ensure_checkpoint(spec, d)
 
 
