@@ -112,8 +112,10 @@ def checkpoint_dir(spec) -> str:
     key = spec_key(spec)
     for base in BENCH_BASES:
         marker = os.path.join(base, spec.name, "bench.key")
-        if os.path.exists(marker) and open(marker).read() == key:
-            return os.path.join(base, spec.name)
+        if os.path.exists(marker):
+            with open(marker) as f:
+                if f.read() == key:
+                    return os.path.join(base, spec.name)
     need = spec.payload_bytes + len(spec.tensors) * spec.alignment + 4096 + (1 << 30)
     for base in BENCH_BASES:
         d = os.path.join(base, spec.name)
@@ -140,7 +142,11 @@ def ensure_checkpoint(spec, d: str):
     while converting, or regenerated if a converted copy has none)."""
     marker = os.path.join(d, "bench.key")
     key = spec_key(spec)
-    if os.path.exists(marker) and open(marker).read() == key:
+    have_key = None
+    if os.path.exists(marker):
+        with open(marker) as f:
+            have_key = f.read()
+    if have_key == key:
         digests = verify.load_digests(d, key, len(spec.tensors))
         if digests is None:
             t0 = time.time()
@@ -161,7 +167,8 @@ def ensure_checkpoint(spec, d: str):
 
     binding.convert(tensors(), d, spec.alignment, spec.chunk_size, fsync=True)
     verify.save_digests(d, key, digests)
-    open(marker, "w").write(key)
+    with open(marker, "w") as f:
+        f.write(key)
     log(f"converted {spec.name} into {d} in {time.time() - t0:.1f} s")
     return digests
 
