@@ -738,116 +738,146 @@ def measure_k2(torch, workload: str, dev_alignment: int, stream, reps: int = 6, 
 
 
 def measure_extras(torch, spec, d, pool, buf, stream, engine):
-    """Other engines and tiers on the same checkpoint (outside the graded step)."""
+    """Other engines and tiers on the same checkpoint (outside the graded
+    step).  Each extra runs on its own: one that fails (a full disk, say)
+    records its error and leaves the others and the graded line intact."""
     out = {}
     T = buf.numel()
+
+    def attempt(name, fn):
+        try:
+            out[name] = fn()
+            log(f"{name}:", out[name])
+        except Exception as e:  # noqa: BLE001
+            out[name] = {"error": f"{type(e).__name__}: {e}"}
+            log(f"{name} failed: {e}")
+
     # the copy-engine path from the same cached chunks
     other = "sdma" if engine == "kernel" else "kernel"
-    times = []
-    for i in range(6):
-        t0 = time.perf_counter()
-        with binding.Checkpoint(d, pool=pool, engine=other) as ck:
-            ck.load_into(buf, stream)
-            stream.synchronize()
-        if i:
-            times.append(time.perf_counter() - t0)
-    out[f"engine_{other}"] = {"time_to_ready_s": round(statistics.median(times), 5),
-                              "GBps": round(T / statistics.median(times) / 1e9, 3)}
-    log("other engine:", out[f"engine_{other}"])
+
+    def other_engine():
+        times = []
+        for i in range(6):
+            t0 = time.perf_counter()
+            with binding.Checkpoint(d, pool=pool, engine=other) as ck:
+                ck.load_into(buf, stream)
+                stream.synchronize()
+            if i:
+                times.append(time.perf_counter() - t0)
+        return {"time_to_ready_s": round(statistics.median(times), 5),
+                "GBps": round(T / statistics.median(times) / 1e9, 3)}
+
+    attempt(f"engine_{other}", other_engine)
     # K2 on repacks that move bytes: the 8 GiB stress prefix (4 KiB file
     # alignment, padding after most tensors) into A2 = 256, and the same
     # tensors packed densely (A = 1), whose shifts need the byte funnel
-    out["repack_k2"] = measure_k2(torch, "stress-8g", 256, stream)
-    log("repack:", out["repack_k2"])
-    out["repack_k2_dense"] = measure_k2(torch, "stress-8g-dense", 256, stream)
-    log("repack (dense file):", out["repack_k2_dense"])
+    attempt("repack_k2", lambda: measure_k2(torch, "stress-8g", 256, stream))
+    attempt("repack_k2_dense", lambda: measure_k2(torch, "stress-8g-dense", 256, stream))
+
     # the 7B image into A2 = 4 KiB: every 7B tensor is a multiple of 8 KiB,
     # so that layout equals the file layout and K2 only copies (an upper
     # bound, every tile straight)
-    with binding.Checkpoint(d, pool=pool, dev_alignment=4096) as ck:
-        T2 = ck.total_bytes
-        dst = torch.empty(T2, dtype=torch.uint8, device="cuda:0")
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ms = []
-        for i in range(6):
-            e0.record(stream)
-            ck.repack(buf, dst, stream)
-            e1.record(stream)
-            e1.synchronize()
-            if i:
-                ms.append(e0.elapsed_time(e1))
+    def identity_copy():
+        with binding.Checkpoint(d, pool=pool, dev_alignment=4096) as ck:
+            T2 = ck.total_bytes
+            dst = torch.empty(T2, dtype=torch.uint8, device="cuda:0")
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            ms = []
+            for i in range(6):
+                e0.record(stream)
+                ck.repack(buf, dst, stream)
+                e1.record(stream)
+                e1.synchronize()
+                if i:
+                    ms.append(e0.elapsed_time(e1))
+            del dst
         k2 = (T + T2) / (statistics.mean(ms) * 1e-3) / 1e9
         k2c = profiled_counters("k2_tiles_repack_llama-2-7b.md", *K2_SOURCES)
-        out["repack_k2_identity_copy"] = {
-            "workload": spec.name, "dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
-            "note": "identity layout (every tensor a multiple of 8 KiB): a copy, not a relocation",
-            "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1), "bound": "hbm",
-            "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),
-            "traffic": (k2c["fetch_bytes_per_launch"] + k2c["write_bytes_per_launch"]) if k2c else None}
-        del dst
-    log("repack (identity copy):", out["repack_k2_identity_copy"])
+        return {"workload": spec.name, "dev_alignment": 4096, "bytes_read": T, "bytes_written": T2,
+                "note": "identity layout (every tensor a multiple of 8 KiB): a copy, not a relocation",
+                "kernel_ms": round(statistics.mean(ms), 3), "achieved_GBps": round(k2, 1), "bound": "hbm",
+                "peak": HBM_PEAK_GBPS, "frac_hbm_peak": round(k2 / HBM_PEAK_GBPS, 4),
+                "traffic": (k2c["fetch_bytes_per_launch"] + k2c["write_bytes_per_launch"]) if k2c else None}
+
+    attempt("repack_k2_identity_copy", identity_copy)
+
     # streamed from the file with direct I/O through a 1 GiB ring, 16 readers
     # (cold: O_DIRECT bypasses the page cache), next to the storage device's
     # own peak measured the way the paper normalizes storage bandwidth
-    slots = max(16, (1 << 30) // spec.chunk_size)
-    with binding.Pool(spec.chunk_size, slots) as ring_pool:
-        with binding.Checkpoint(d, pool=ring_pool, engine=engine, direct_io=True, io_threads=16,
-                                ring_slots=slots) as ck:
-            t0 = time.perf_counter()
-            ck.load_into(buf, stream)
-            stream.synchronize()
-            dt = time.perf_counter() - t0
-            st = ck.stats()
-    peak = storage_peak(os.path.join(d, "sllm.part0"))
-    out["file_direct_ring"] = {"GBps": round(T / dt / 1e9, 3), "s": round(dt, 3), "direct_io": int(st["direct_io"]),
-                               "io_threads": 16, "ring_slots": slots, "read_wait_s": round(st["read_wait_s"], 3),
-                               "device": block_device(d), "storage_peak_GBps": peak["GBps"] if peak else None}
-    log("file ring:", out["file_direct_ring"])
+    def direct_ring():
+        slots = max(16, (1 << 30) // spec.chunk_size)
+        with binding.Pool(spec.chunk_size, slots) as ring_pool:
+            with binding.Checkpoint(d, pool=ring_pool, engine=engine, direct_io=True, io_threads=16,
+                                    ring_slots=slots) as ck:
+                t0 = time.perf_counter()
+                ck.load_into(buf, stream)
+                stream.synchronize()
+                dt = time.perf_counter() - t0
+                st = ck.stats()
+        peak = storage_peak(os.path.join(d, "sllm.part0"))
+        return {"GBps": round(T / dt / 1e9, 3), "s": round(dt, 3), "direct_io": int(st["direct_io"]),
+                "io_threads": 16, "ring_slots": slots, "read_wait_s": round(st["read_wait_s"], 3),
+                "device": block_device(d), "storage_peak_GBps": peak["GBps"] if peak else None}
+
+    attempt("file_direct_ring", direct_ring)
+
     # the tiers in one pass: a first load straight from the file (O_DIRECT)
     # that leaves the partition cached in the pool (SLLM_OPEN_CACHE), then a
     # load of the same handle from that cache
-    pool.evict(d)
-    t0 = time.perf_counter()
-    with binding.Checkpoint(d, pool=pool, engine=engine, cache=True, direct_io=True, io_threads=16) as ck:
-        ck.load_into(buf, stream)
-        stream.synchronize()
-        t1 = time.perf_counter()
-        first = ck.stats()
-        ck.load_into(buf, stream)
-        stream.synchronize()
-        t2 = time.perf_counter()
-        second = ck.stats()
-    out["file_direct_then_cached"] = {
-        "first_GBps": round(T / (t1 - t0) / 1e9, 3), "first_s": round(t1 - t0, 3),
-        "first_from_cache": int(first["from_cache"]), "second_GBps": round(T / (t2 - t1) / 1e9, 3),
-        "second_from_cache": int(second["from_cache"]), "cached_after": pool.info()["cached_checkpoints"]}
-    log("file then cached:", out["file_direct_then_cached"])
+    def direct_then_cached():
+        pool.evict(d)
+        try:
+            t0 = time.perf_counter()
+            with binding.Checkpoint(d, pool=pool, engine=engine, cache=True, direct_io=True, io_threads=16) as ck:
+                ck.load_into(buf, stream)
+                stream.synchronize()
+                t1 = time.perf_counter()
+                first = ck.stats()
+                ck.load_into(buf, stream)
+                stream.synchronize()
+                t2 = time.perf_counter()
+                second = ck.stats()
+        finally:
+            if not pool.info()["cached_checkpoints"]:  # leave the partition cached, as found
+                pool.cache(d)
+        return {"first_GBps": round(T / (t1 - t0) / 1e9, 3), "first_s": round(t1 - t0, 3),
+                "first_from_cache": int(first["from_cache"]), "second_GBps": round(T / (t2 - t1) / 1e9, 3),
+                "second_from_cache": int(second["from_cache"]), "cached_after": pool.info()["cached_checkpoints"]}
+
+    attempt("file_direct_then_cached", direct_then_cached)
+
     # the one-time conversion (Sec. 4.1; reported, not graded): the first
     # tensors of the workload, about 1 GiB held in memory, written by the
-    # batch converter and by the streaming writer, each with fsync
-    import shutil
-    import tempfile
+    # batch converter and by the streaming writer, each with fsync, on the
+    # checkpoint's file system if it has room for both copies
+    def convert():
+        import tempfile
 
-    k, nbytes = 0, 0
-    while k < len(spec.tensors) and nbytes < (1 << 30):
-        nbytes += spec.tensors[k].nbytes
-        k += 1
-    sub = [(t.name, t.dtype, t.shape, data) for _, t, data in synth.iter_tensors(spec, indices=range(k))]
-    tmp = tempfile.mkdtemp(dir=os.path.dirname(os.path.abspath(d)))
-    try:
-        t0 = time.perf_counter()
-        binding.convert_array(sub, os.path.join(tmp, "batch"), spec.alignment, spec.chunk_size, fsync=True)
-        t_batch = time.perf_counter() - t0
-        t0 = time.perf_counter()
-        binding.convert(iter(sub), os.path.join(tmp, "stream"), spec.alignment, spec.chunk_size, fsync=True)
-        t_stream = time.perf_counter() - t0
-    finally:
-        shutil.rmtree(tmp, ignore_errors=True)
-    del sub
-    out["convert"] = {"tensors": k, "bytes": nbytes, "batch_GBps": round(nbytes / t_batch / 1e9, 3),
-                      "streaming_GBps": round(nbytes / t_stream / 1e9, 3), "fsync": True,
-                      "device": block_device(d)}
-    log("convert:", out["convert"])
+        k, nbytes = 0, 0
+        while k < len(spec.tensors) and nbytes < (1 << 30):
+            nbytes += spec.tensors[k].nbytes
+            k += 1
+        need = 2 * (nbytes + k * spec.alignment + 4096) + (1 << 30)
+        bases = [os.path.dirname(os.path.abspath(d))] + list(BENCH_BASES)
+        base = next((b for b in bases if _free_bytes(b) >= need), None)
+        if base is None:
+            return {"skipped": f"no file system with {need} bytes free for the two copies"}
+        os.makedirs(base, exist_ok=True)
+        sub = [(t.name, t.dtype, t.shape, data) for _, t, data in synth.iter_tensors(spec, indices=range(k))]
+        tmp = tempfile.mkdtemp(dir=base)
+        try:
+            t0 = time.perf_counter()
+            binding.convert_array(sub, os.path.join(tmp, "batch"), spec.alignment, spec.chunk_size, fsync=True)
+            t_batch = time.perf_counter() - t0
+            t0 = time.perf_counter()
+            binding.convert(iter(sub), os.path.join(tmp, "stream"), spec.alignment, spec.chunk_size, fsync=True)
+            t_stream = time.perf_counter() - t0
+        finally:
+            shutil.rmtree(tmp, ignore_errors=True)
+        return {"tensors": k, "bytes": nbytes, "batch_GBps": round(nbytes / t_batch / 1e9, 3),
+                "streaming_GBps": round(nbytes / t_stream / 1e9, 3), "fsync": True, "device": block_device(base)}
+
+    attempt("convert", convert)
     return out
 
 
@@ -1040,9 +1070,13 @@ def main():
         storage = storage_peak(os.path.join(d, "sllm.part0"))
         extras["storage_peak"] = storage
     tiers = binding.TIER_DRAM | (0 if cached else binding.TIER_STORAGE)
-    extras["estimator"] = estimator_online(d, open_kw, buf, stream, T, tiers, (h2d_peak or 50.0) * 1e9,
-                                           (storage["GBps"] if storage else 5.0) * 1e9,
-                                           loads=10 if cached else 3)
+    try:
+        extras["estimator"] = estimator_online(d, open_kw, buf, stream, T, tiers, (h2d_peak or 50.0) * 1e9,
+                                               (storage["GBps"] if storage else 5.0) * 1e9,
+                                               loads=10 if cached else 3)
+    except Exception as e:  # noqa: BLE001  (an extra: the graded line still prints)
+        extras["estimator"] = {"error": f"{type(e).__name__}: {e}"}
+        log(f"estimator failed: {e}")
     if tracing:
         extras["timeline"] = timeline_summary(args.trace, T)
     if not cached:
